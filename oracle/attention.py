@@ -1,0 +1,188 @@
+"""fp64 eviction-masked attention: the definition, written out (test infrastructure).
+
+Section 2 ("KV-streams") keeps every retained key and value at its original
+position and replaces the deletion of a span by an attention mask in a single
+pass over the continuous trace; the engine drops evicted keys and values for
+good and the trainer mirrors the drop with a mask (Section 7, second
+paragraph), so each key ``j`` of a trace has one eviction index ``e_j`` and
+query ``i`` attends to it iff
+
+    j <= i < e_j            (any e_j >= L means "never evicted").
+
+For one trace of length L, q-head h and its KV head g = h // (Hq // Hkv):
+
+    V(i)    = { j : j <= i < min(e_j, L) }
+    s_ij    = scale * <q_i^h, k_j^g>
+    LSE_i   = ln sum_{j in V(i)} exp(s_ij)
+    P_ij    = exp(s_ij - LSE_i)  on V(i), else 0
+    O_i     = sum_j P_ij v_j^g
+
+and for the scalar loss sum(dO * O):
+
+    dP_ij   = <dO_i, v_j^g>
+    Delta_i = sum_j P_ij dP_ij
+    dS_ij   = P_ij (dP_ij - Delta_i)
+    dQ_i    = scale sum_j dS_ij k_j^g
+    dK_j^g  = scale sum_{h in g} sum_i dS_ij q_i^h
+    dV_j^g  = sum_{h in g} sum_i P_ij dO_i^h
+
+The mask is built explicitly as a boolean matrix; the softmax is two-pass
+(row max, then sum) over the full causal prefix of each block of query rows.
+Nothing is skipped.  Inputs are the exact bf16 values widened to fp64.
+
+Parity of every function here is pinned by tests against causal attention
+(``e = inf``), a brute-force stream replay, finite differences, closed forms
+and hand counts; see the module ``tests/test_oracle_pins.py``.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+ROW_BLOCK = 256
+
+
+def _f64(x) -> np.ndarray:
+    if hasattr(x, "detach"):  # torch tensor (bf16 or float)
+        import torch
+
+        return x.detach().to(torch.float64).cpu().numpy()
+    return np.asarray(x, dtype=np.float64)
+
+
+def visible_mask(e: np.ndarray, L: int, i0: int, i1: int, j1: int) -> np.ndarray:
+    """Boolean mask of rows ``[i0, i1)`` by columns ``[0, j1)``: ``j <= i < min(e_j, L)``."""
+    i = np.arange(i0, i1)[:, None]
+    j = np.arange(0, j1)[None, :]
+    ej = np.minimum(e[:j1].astype(np.int64), L)[None, :]
+    return (j <= i) & (i < ej)
+
+
+def check_evict_at(e: np.ndarray, L: int) -> None:
+    """Every key must be visible to itself: ``e_j > j``."""
+    e = np.asarray(e, dtype=np.int64)
+    if e.shape != (L,):
+        raise ValueError(f"evict_at has shape {e.shape}, expected ({L},)")
+    bad = np.nonzero(e <= np.arange(L))[0]
+    if bad.size:
+        raise ValueError(f"evict_at[{bad[0]}] = {e[bad[0]]} <= {bad[0]}")
+
+
+def _trace_forward(q, k, v, e, scale):
+    """One trace: q [L,Hq,D], k/v [L,Hkv,D] fp64, e [L]. Returns O [L,Hq,D], LSE [Hq,L]."""
+    L, Hq, D = q.shape
+    Hkv = k.shape[1]
+    G = Hq // Hkv
+    O = np.zeros((L, Hq, v.shape[2]))
+    LSE = np.zeros((Hq, L))
+    for h in range(Hq):
+        g = h // G
+        for i0 in range(0, L, ROW_BLOCK):
+            i1 = min(i0 + ROW_BLOCK, L)
+            M = visible_mask(e, L, i0, i1, i1)
+            S = scale * (q[i0:i1, h, :] @ k[:i1, g, :].T)
+            S = np.where(M, S, -np.inf)
+            m = S.max(axis=1, keepdims=True)
+            E = np.where(M, np.exp(S - m), 0.0)
+            l = E.sum(axis=1, keepdims=True)
+            P = E / l
+            O[i0:i1, h, :] = P @ v[:i1, g, :]
+            LSE[h, i0:i1] = (m + np.log(l))[:, 0]
+    return O, LSE
+
+
+def _trace_backward(q, k, v, e, scale, do):
+    """One trace: returns O, LSE, Delta [Hq,L], dQ, dK, dV (fp64)."""
+    L, Hq, D = q.shape
+    Hkv = k.shape[1]
+    G = Hq // Hkv
+    O = np.zeros((L, Hq, v.shape[2]))
+    LSE = np.zeros((Hq, L))
+    Delta = np.zeros((Hq, L))
+    dq = np.zeros_like(q)
+    dk = np.zeros_like(k)
+    dv = np.zeros_like(v)
+    for h in range(Hq):
+        g = h // G
+        for i0 in range(0, L, ROW_BLOCK):
+            i1 = min(i0 + ROW_BLOCK, L)
+            M = visible_mask(e, L, i0, i1, i1)
+            S = scale * (q[i0:i1, h, :] @ k[:i1, g, :].T)
+            S = np.where(M, S, -np.inf)
+            m = S.max(axis=1, keepdims=True)
+            E = np.where(M, np.exp(S - m), 0.0)
+            l = E.sum(axis=1, keepdims=True)
+            P = E / l
+            O[i0:i1, h, :] = P @ v[:i1, g, :]
+            LSE[h, i0:i1] = (m + np.log(l))[:, 0]
+            dP = do[i0:i1, h, :] @ v[:i1, g, :].T
+            dlt = (P * dP).sum(axis=1, keepdims=True)
+            Delta[h, i0:i1] = dlt[:, 0]
+            dS = P * (dP - dlt)
+            dq[i0:i1, h, :] = scale * (dS @ k[:i1, g, :])
+            dk[:i1, g, :] += scale * (dS.T @ q[i0:i1, h, :])
+            dv[:i1, g, :] += P.T @ do[i0:i1, h, :]
+    return O, LSE, Delta, dq, dk, dv
+
+
+def _split(cu_seqlens, n):
+    if cu_seqlens is None:
+        return [(0, n)]
+    cu = [int(c) for c in cu_seqlens]
+    return [(cu[b], cu[b + 1]) for b in range(len(cu) - 1)]
+
+
+def forward(q, k, v, evict_at, scale, cu_seqlens=None):
+    """Packed traces ``[ntok, H, D]`` (``cu_seqlens`` = trace offsets; None = one trace).
+
+    ``evict_at`` is trace-local.  Returns fp64 ``O [ntok,Hq,D]`` and ``LSE [Hq,ntok]``.
+    """
+    q, k, v = _f64(q), _f64(k), _f64(v)
+    e = np.asarray(evict_at, dtype=np.int64)
+    n, Hq, _ = q.shape
+    if k.shape[0] != n or v.shape[0] != n or e.shape != (n,) or Hq % k.shape[1]:
+        raise ValueError("shape mismatch")
+    O = np.zeros((n, Hq, v.shape[2]))
+    LSE = np.zeros((Hq, n))
+    for a, b in _split(cu_seqlens, n):
+        if b == a:
+            continue
+        check_evict_at(e[a:b], b - a)
+        O[a:b], LSE[:, a:b] = _trace_forward(q[a:b], k[a:b], v[a:b], e[a:b], scale)
+    return O, LSE
+
+
+def backward(q, k, v, evict_at, scale, do, cu_seqlens=None):
+    """Gradients of ``sum(do * O)``; returns dict with O, LSE, Delta, dq, dk, dv (fp64)."""
+    q, k, v, do = _f64(q), _f64(k), _f64(v), _f64(do)
+    e = np.asarray(evict_at, dtype=np.int64)
+    n, Hq, _ = q.shape
+    if k.shape[0] != n or v.shape[0] != n or e.shape != (n,) or do.shape != (n, Hq, v.shape[2]):
+        raise ValueError("shape mismatch")
+    out = {
+        "O": np.zeros((n, Hq, v.shape[2])),
+        "LSE": np.zeros((Hq, n)),
+        "Delta": np.zeros((Hq, n)),
+        "dq": np.zeros_like(q),
+        "dk": np.zeros_like(k),
+        "dv": np.zeros_like(v),
+    }
+    for a, b in _split(cu_seqlens, n):
+        if b == a:
+            continue
+        check_evict_at(e[a:b], b - a)
+        O, LSE, Dl, dq, dk, dv = _trace_backward(q[a:b], k[a:b], v[a:b], e[a:b], scale, do[a:b])
+        out["O"][a:b], out["LSE"][:, a:b], out["Delta"][:, a:b] = O, LSE, Dl
+        out["dq"][a:b], out["dk"][a:b], out["dv"][a:b] = dq, dk, dv
+    return out
+
+
+def visible_pairs(evict_at, lengths) -> int:
+    """Visible (query, key) pairs per head, counted from the explicit mask row by row."""
+    e = np.asarray(evict_at, dtype=np.int64)
+    tot, off = 0, 0
+    for L in lengths:
+        for i0 in range(0, L, ROW_BLOCK):
+            i1 = min(i0 + ROW_BLOCK, L)
+            tot += int(visible_mask(e[off:off + L], L, i0, i1, i1).sum())
+        off += L
+    return tot

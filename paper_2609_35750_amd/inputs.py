@@ -1,0 +1,197 @@
+"""Seeded synthetic inputs for eviction-masked attention.
+
+This module builds the two kinds of input that both the HIP path and the
+CPU checker consume, and nothing else: the per-key eviction index
+``evict_at`` of a compacted agent trace, and seeded bf16 Q/K/V/dO tensors.
+It holds none of the attention arithmetic.
+
+Trace layout (Section 2, "KV-streams"; Section 3, "Summary"; Appendix B,
+"Turn-Wise Compaction").  A trace of length ``L`` starts with a prompt
+``[0, p)`` that is never evicted.  Segment ``k`` starts at ``a_k`` with
+``a_0 = p`` and ``a_{k+1} = a_k + w + s``; it holds ``w`` turn tokens
+``U_k = [a_k, a_k + w)`` followed by an ``s``-token summary
+``S_k = [a_k + w, a_{k+1})`` (both clipped to ``[0, L)``).  Compaction ``k``
+happens only once its summary is complete (``a_{k+1} <= L``): the summary is
+generated while the turns are still visible, then the whole turns are
+deleted, so ``evict_at[U_k] = a_{k+1}``.  Turns of a segment whose summary is
+cut off by the end of the trace are never evicted.
+
+Summary retention strategies:
+
+* ``keep_all``     every summary stays for the rest of the trace;
+* ``latest_only``  summary ``S_k`` is deleted when ``S_{k+1}`` completes,
+                   i.e. ``evict_at[S_k] = a_{k+2}``;
+* ``last2``        only the two newest summaries stay: ``S_k`` is deleted
+                   when ``S_{k+2}`` completes, ``evict_at[S_k] = a_{k+3}``.
+
+A key that is never evicted carries ``evict_at = L`` (any value ``>= L``
+means the same).  Query ``i`` sees key ``j`` iff ``j <= i < evict_at[j]``.
+
+Tensor recipe: fp32 standard normal draws from a seeded CPU
+``torch.Generator`` (one seed per tensor), rounded to bf16 with
+round-to-nearest-even.  Where a workload states that Q is pre-scaled by
+``1/sqrt(D)``, Q is drawn as ``N(0,1)/sqrt(D)`` before rounding and the
+softmax scale is 1.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+
+STRATEGIES = ("keep_all", "latest_only", "last2")
+
+
+def segment_starts(L: int, p: int, w: int, s: int) -> List[int]:
+    """Start positions ``a_0, a_1, ...`` of every segment that begins before ``L``,
+    plus one more start past the last one (so ``a_{k+1}`` always exists)."""
+    if w + s <= 0:
+        raise ValueError("segment length w + s must be positive")
+    a = [p]
+    while a[-1] < L:
+        a.append(a[-1] + w + s)
+    a.append(a[-1] + w + s)
+    return a
+
+
+def evict_at_layout(L: int, p: int, w: int, s: int, strategy: str = "keep_all") -> np.ndarray:
+    """``evict_at`` (int32, length ``L``) of one trace built from the segment layout."""
+    if strategy not in STRATEGIES:
+        raise ValueError(f"unknown strategy {strategy!r}")
+    if L < 1 or p < 0 or w < 0 or s < 0:
+        raise ValueError("bad layout")
+    e = np.full(L, L, dtype=np.int64)
+    a = segment_starts(L, p, w, s)
+    nseg = len(a) - 2
+
+    def fired(k: int) -> bool:  # compaction k happens iff its summary completes inside the trace
+        return 0 <= k < nseg and a[k + 1] <= L
+
+    for k in range(nseg):
+        if fired(k):
+            e[a[k]:min(a[k] + w, L)] = a[k + 1]
+        lo, hi = a[k] + w, min(a[k + 1], L)
+        if lo >= hi:
+            continue
+        if strategy == "latest_only" and fired(k + 1):
+            e[lo:hi] = a[k + 2]
+        elif strategy == "last2" and fired(k + 2):
+            e[lo:hi] = a[k + 3]
+    return np.minimum(e, L).astype(np.int32)
+
+
+def evict_at_random(L: int, rng: np.random.Generator, p_never: float = 0.3) -> np.ndarray:
+    """Unstructured valid eviction indices: ``e_j`` uniform on ``(j, L]`` (``L`` = never)."""
+    e = np.empty(L, dtype=np.int64)
+    for j in range(L):
+        e[j] = L if rng.random() < p_never else rng.integers(j + 1, L + 1)
+    return e.astype(np.int32)
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    """One synthetic workload shaped like an agent trace batch."""
+
+    name: str
+    Hq: int
+    Hkv: int
+    D: int
+    lengths: tuple
+    p: int
+    w: int
+    s: int
+    strategy: str
+    q_prescaled: bool
+    varlen: bool
+    seed: int
+
+    @property
+    def B(self) -> int:
+        return len(self.lengths)
+
+    @property
+    def T(self) -> int:
+        return max(self.lengths)
+
+    @property
+    def ntok(self) -> int:
+        return int(sum(self.lengths))
+
+    @property
+    def G(self) -> int:
+        return self.Hq // self.Hkv
+
+    @property
+    def softmax_scale(self) -> float:
+        return 1.0 if self.q_prescaled else 1.0 / math.sqrt(self.D)
+
+    def evict_at(self) -> np.ndarray:
+        """Trace-local eviction indices, concatenated in trace order (int32, ``[ntok]``)."""
+        return np.concatenate([evict_at_layout(L, self.p, self.w, self.s, self.strategy) for L in self.lengths])
+
+    def cu_seqlens(self) -> np.ndarray:
+        return np.concatenate([[0], np.cumsum(self.lengths)]).astype(np.int32)
+
+
+def varlen_lengths(n: int, lo: int, hi: int, seed: int) -> tuple:
+    """Trace lengths drawn i.i.d. uniform on ``[lo, hi]`` (inclusive) from a seeded numpy generator."""
+    return tuple(int(x) for x in np.random.default_rng(seed).integers(lo, hi, n, endpoint=True))
+
+
+def _workloads() -> Dict[str, Workload]:
+    W = Workload
+    return {
+        w.name: w
+        for w in [
+            W("trace512_tiny", 4, 4, 64, (512,), 64, 128, 32, "keep_all", False, False, 1001),
+            W("trace16k_gqa4", 32, 8, 128, (16384,), 1024, 4096, 512, "keep_all", True, False, 1002),
+            W("trace32k_latest", 32, 8, 128, (32768,), 1024, 3072, 256, "latest_only", False, False, 1003),
+            W("varlen8_gqa5", 40, 8, 128, varlen_lengths(8, 4096, 24576, 39), 512, 2048, 256, "keep_all", False, True, 1004),
+            W("trace64k_last2", 64, 8, 128, (65536,), 2048, 2048, 256, "last2", False, False, 1005),
+        ]
+    }
+
+
+WORKLOADS: Dict[str, Workload] = _workloads()
+WORKLOAD_ORDER = ["trace512_tiny", "trace16k_gqa4", "trace32k_latest", "varlen8_gqa5", "trace64k_last2"]
+
+
+def custom_workload(name: str, Hq: int, Hkv: int, D: int, lengths: Sequence[int], p: int, w: int, s: int,
+                    strategy: str = "keep_all", q_prescaled: bool = False, varlen: Optional[bool] = None,
+                    seed: int = 0) -> Workload:
+    if varlen is None:
+        varlen = len(lengths) > 1 and len(set(lengths)) > 1
+    return Workload(name, Hq, Hkv, D, tuple(int(x) for x in lengths), p, w, s, strategy, q_prescaled, varlen, seed)
+
+
+def randn_bf16(shape, seed: int, scale: float = 1.0):
+    """bf16 tensor of ``N(0,1) * scale`` draws (fp32 draw, one rounding to bf16), on the CPU."""
+    import torch
+
+    g = torch.Generator(device="cpu")
+    g.manual_seed(int(seed))
+    x = torch.randn(*shape, generator=g, dtype=torch.float32)
+    if scale != 1.0:
+        x = x * scale
+    return x.to(torch.bfloat16)
+
+
+def make_tensors(wl: Workload, with_grad: bool = True):
+    """Seeded bf16 CPU tensors ``q, k, v`` (and ``do``) for a workload.
+
+    Packed layout ``[ntok, H, D]``; a fixed-length batch of ``B`` traces of
+    length ``T`` is the same memory as ``[B, T, H, D]``.
+    """
+    n = wl.ntok
+    qs = 1.0 / math.sqrt(wl.D) if wl.q_prescaled else 1.0
+    out = {
+        "q": randn_bf16((n, wl.Hq, wl.D), wl.seed * 16 + 1, qs),
+        "k": randn_bf16((n, wl.Hkv, wl.D), wl.seed * 16 + 2),
+        "v": randn_bf16((n, wl.Hkv, wl.D), wl.seed * 16 + 3),
+    }
+    if with_grad:
+        out["do"] = randn_bf16((n, wl.Hq, wl.D), wl.seed * 16 + 4)
+    return out
+

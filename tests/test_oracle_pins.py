@@ -1,0 +1,274 @@
+"""Pins of the fp64 CPU checker against facts that do not come from itself.
+
+Each test ties the checker (``oracle/``) to something else the paper or the
+mathematics fixes: causal attention from a library routine, a token-by-token
+replay of the streamed KV cache, finite differences, closed forms and hand
+counts.  No GPU.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import attention as orc
+from oracle import stream_sim, tiles
+from paper_2609_35750_amd import inputs
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+BIG = np.iinfo(np.int32).max
+
+
+def _rand(shape, seed, scale=1.0):
+    return inputs.randn_bf16(shape, seed, scale)
+
+
+def _sdpa_causal(q, k, v, scale):
+    """torch SDPA on fp64 CPU tensors [L,H,D] -> O [L,Hq,D], with GQA."""
+    qt, kt, vt = (x.permute(1, 0, 2).unsqueeze(0) for x in (q, k, v))
+    o = torch.nn.functional.scaled_dot_product_attention(qt, kt, vt, is_causal=True, scale=scale, enable_gqa=True)
+    return o.squeeze(0).permute(1, 0, 2)
+
+
+def _f64t(x):
+    return x.to(torch.float64).clone().requires_grad_(True)
+
+
+# ---------------------------------------------------------------- P1: e = inf is causal attention
+@pytest.mark.parametrize("L,Hq,Hkv,D", [(97, 4, 2, 16), (33, 3, 1, 8), (64, 2, 2, 32)])
+def test_never_evicted_equals_causal_sdpa(L, Hq, Hkv, D):
+    q, k, v, do = _rand((L, Hq, D), 1), _rand((L, Hkv, D), 2), _rand((L, Hkv, D), 3), _rand((L, Hq, D), 4)
+    scale = 1.0 / math.sqrt(D)
+    e = np.full(L, BIG, dtype=np.int64)
+    res = orc.backward(q, k, v, e, scale, do)
+    qt, kt, vt = _f64t(q), _f64t(k), _f64t(v)
+    o = _sdpa_causal(qt, kt, vt, scale)
+    (o * do.to(torch.float64)).sum().backward()
+    np.testing.assert_allclose(res["O"], o.detach().numpy(), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(res["dq"], qt.grad.numpy(), rtol=1e-10, atol=1e-11)
+    np.testing.assert_allclose(res["dk"], kt.grad.numpy(), rtol=1e-10, atol=1e-11)
+    np.testing.assert_allclose(res["dv"], vt.grad.numpy(), rtol=1e-10, atol=1e-11)
+    # LSE: logsumexp of the causal row, independent of the masked path
+    s = torch.einsum("ihd,jhd->hij", q.double(), k.double().repeat_interleave(Hq // Hkv, dim=1)) * scale
+    s = s.masked_fill(~torch.ones(L, L, dtype=torch.bool).tril(), -math.inf)
+    np.testing.assert_allclose(res["LSE"], torch.logsumexp(s, dim=-1).numpy(), rtol=1e-12, atol=1e-12)
+    fo, flse = orc.forward(q, k, v, e, scale)
+    np.testing.assert_array_equal(fo, res["O"])
+    np.testing.assert_array_equal(flse, res["LSE"])
+
+
+# ---------------------------------------------------------------- P2: brute-force stream replay
+def _replay_check(L, p, w, s, strategy, Hq, Hkv, D, seed, grads=True):
+    q, k, v, do = _rand((L, Hq, D), seed), _rand((L, Hkv, D), seed + 1), _rand((L, Hkv, D), seed + 2), _rand((L, Hq, D), seed + 3)
+    scale = 1.0 / math.sqrt(D)
+    qt, kt, vt = _f64t(q), _f64t(k), _f64t(v)
+    O, LSE, lives = stream_sim.replay(qt, kt, vt, p, w, s, strategy, scale, return_live=True)
+    # the layout rules reproduce exactly the replayed live sets
+    e_sim = stream_sim.live_sets_to_evict_at(lives, L)
+    e = inputs.evict_at_layout(L, p, w, s, strategy)
+    np.testing.assert_array_equal(np.minimum(e, L), e_sim)
+    res = orc.backward(q, k, v, e, scale, do)
+    np.testing.assert_allclose(res["O"], O.detach().numpy(), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(res["LSE"], LSE.detach().numpy(), rtol=1e-12, atol=1e-12)
+    if grads:
+        (O * do.to(torch.float64)).sum().backward()
+        np.testing.assert_allclose(res["dq"], qt.grad.numpy(), rtol=1e-9, atol=1e-10)
+        np.testing.assert_allclose(res["dk"], kt.grad.numpy(), rtol=1e-9, atol=1e-10)
+        np.testing.assert_allclose(res["dv"], vt.grad.numpy(), rtol=1e-9, atol=1e-10)
+
+
+def test_replay_matches_tiny_keep_all_trace():
+    wl = inputs.WORKLOADS["trace512_tiny"]
+    _replay_check(512, wl.p, wl.w, wl.s, wl.strategy, 4, 4, 64, seed=11, grads=False)
+
+
+@pytest.mark.parametrize("strategy", inputs.STRATEGIES)
+@pytest.mark.parametrize("case", range(4))
+def test_replay_matches_random_layouts(strategy, case):
+    rng = np.random.default_rng(100 + case)
+    L = int(rng.integers(30, 140))
+    p, w, s = int(rng.integers(0, 12)), int(rng.integers(1, 20)), int(rng.integers(0, 8))
+    G = [1, 2, 3][case % 3]
+    _replay_check(L, p, w, s, strategy, Hq=2 * G, Hkv=2, D=8, seed=200 + case)
+
+
+# ---------------------------------------------------------------- P3: normalisation and masking
+def test_rows_normalise_and_masked_keys_do_not_matter():
+    L, Hq, Hkv, D = 120, 4, 2, 16
+    rng = np.random.default_rng(5)
+    e = inputs.evict_at_random(L, rng)
+    q, k, v = _rand((L, Hq, D), 21), _rand((L, Hkv, D), 22), _rand((L, Hkv, D), 23)
+    scale = 0.3
+    O, LSE = orc.forward(q, k, v, e, scale)
+    qd, kd = q.double().numpy(), k.double().numpy()
+    G = Hq // Hkv
+    for h in range(Hq):
+        for i in range(L):
+            js = [j for j in range(i + 1) if i < e[j]]
+            sc = scale * kd[js, h // G, :] @ qd[i, h, :]
+            assert abs(np.exp(sc - LSE[h, i]).sum() - 1.0) < 1e-12
+    # keys invisible to query i cannot influence row i
+    i = L - 1
+    hidden = [j for j in range(L) if not (j <= i < e[j])]
+    k2, v2 = k.clone(), v.clone()
+    k2[hidden] = _rand((len(hidden), Hkv, D), 99)
+    v2[hidden] = _rand((len(hidden), Hkv, D), 98)
+    O2, LSE2 = orc.forward(q, k2, v2, e, scale)
+    np.testing.assert_array_equal(O2[i], O[i])
+    np.testing.assert_array_equal(LSE2[:, i], LSE[:, i])
+    assert len(hidden) > 10
+
+
+# ---------------------------------------------------------------- P4: finite differences
+@pytest.mark.parametrize("L", [16, 37])
+def test_backward_matches_finite_differences(L):
+    Hq, Hkv, D = 4, 2, 8
+    rng = np.random.default_rng(L)
+    e = inputs.evict_at_random(L, rng)
+    q = torch.from_numpy(rng.standard_normal((L, Hq, D)))
+    k = torch.from_numpy(rng.standard_normal((L, Hkv, D)))
+    v = torch.from_numpy(rng.standard_normal((L, Hkv, D)))
+    do = rng.standard_normal((L, Hq, D))
+    scale = 0.4
+    res = orc.backward(q, k, v, e, scale, do)
+
+    def loss(qq, kk, vv):
+        O, _ = orc.forward(qq, kk, vv, e, scale)
+        return float((O * do).sum())
+
+    eps = 1e-5
+    for name, x, g in (("q", q, res["dq"]), ("k", k, res["dk"]), ("v", v, res["dv"])):
+        num = np.zeros(x.shape)
+        flat = x.numpy().reshape(-1)
+        for idx in range(flat.size):
+            old = flat[idx]
+            flat[idx] = old + eps
+            lp = loss(q, k, v)
+            flat[idx] = old - eps
+            lm = loss(q, k, v)
+            flat[idx] = old
+            num.reshape(-1)[idx] = (lp - lm) / (2 * eps)
+        err = np.abs(num - g).max() / max(1.0, np.abs(g).max())
+        assert err < 1e-6, (name, err)
+
+
+# ---------------------------------------------------------------- P5: closed form, every key lives one step
+def test_self_only_closed_form():
+    L, Hq, Hkv, D = 50, 6, 2, 16
+    q, k, v, do = _rand((L, Hq, D), 31), _rand((L, Hkv, D), 32), _rand((L, Hkv, D), 33), _rand((L, Hq, D), 34)
+    e = np.arange(1, L + 1)
+    scale = 0.25
+    res = orc.backward(q, k, v, e, scale, do)
+    G = Hq // Hkv
+    qd, kd, vd, dod = (x.double().numpy() for x in (q, k, v, do))
+    for h in range(Hq):
+        np.testing.assert_allclose(res["O"][:, h], vd[:, h // G], rtol=0, atol=1e-14)
+        np.testing.assert_allclose(res["LSE"][h], scale * (qd[:, h] * kd[:, h // G]).sum(-1), rtol=1e-13, atol=1e-13)
+    assert np.abs(res["dq"]).max() < 1e-13 and np.abs(res["dk"]).max() < 1e-13
+    np.testing.assert_allclose(res["dv"], dod.reshape(L, Hkv, G, D).sum(2), rtol=1e-13, atol=1e-13)
+
+
+# ---------------------------------------------------------------- P6: nothing retained -> independent segments
+def test_nothing_retained_is_block_diagonal_causal():
+    L, Hq, Hkv, D = 90, 4, 2, 16
+    bounds = [0, 17, 40, 41, 77, 90]
+    e = np.zeros(L, dtype=np.int64)
+    for a, b in zip(bounds[:-1], bounds[1:]):
+        e[a:b] = b
+    q, k, v, do = _rand((L, Hq, D), 41), _rand((L, Hkv, D), 42), _rand((L, Hkv, D), 43), _rand((L, Hq, D), 44)
+    scale = 1.0 / 4
+    res = orc.backward(q, k, v, e, scale, do)
+    for a, b in zip(bounds[:-1], bounds[1:]):
+        qt, kt, vt = _f64t(q[a:b]), _f64t(k[a:b]), _f64t(v[a:b])
+        o = _sdpa_causal(qt, kt, vt, scale)
+        (o * do[a:b].double()).sum().backward()
+        np.testing.assert_allclose(res["O"][a:b], o.detach().numpy(), rtol=1e-12, atol=1e-12)
+        np.testing.assert_allclose(res["dk"][a:b], kt.grad.numpy(), rtol=1e-10, atol=1e-11)
+        np.testing.assert_allclose(res["dv"][a:b], vt.grad.numpy(), rtol=1e-10, atol=1e-11)
+        np.testing.assert_allclose(res["dq"][a:b], qt.grad.numpy(), rtol=1e-10, atol=1e-11)
+
+
+# ---------------------------------------------------------------- retrieval mask of Appendix D
+def test_retrieval_answer_does_not_see_assignment():
+    # [0,4) system prompt, [4,10) assignment turn, [10,26) decoded sequence, [26,32) answer;
+    # the assignment turn is evicted before the first answer token (Appendix D).
+    L, H, D = 32, 2, 16
+    e = np.full(L, L, dtype=np.int64)
+    e[4:10] = 26
+    q, k, v = _rand((L, H, D), 51), _rand((L, H, D), 52), _rand((L, H, D), 53)
+    O, _ = orc.forward(q, k, v, e, 0.25)
+    keep = [j for j in range(L) if not 4 <= j < 10]
+    for i in range(26, L):
+        cols = [j for j in keep if j <= i]
+        mask = torch.zeros(1, L, dtype=torch.bool)
+        mask[0, cols] = True
+        o = torch.nn.functional.scaled_dot_product_attention(
+            q[i:i + 1].double().permute(1, 0, 2), k.double().permute(1, 0, 2), v.double().permute(1, 0, 2),
+            attn_mask=mask, scale=0.25)
+        np.testing.assert_allclose(O[i], o.permute(1, 0, 2)[0].numpy(), rtol=1e-12, atol=1e-12)
+    # before eviction the decoded tokens still see the assignment
+    assert np.abs(O[20] - orc.forward(q, k, v, np.full(L, L), 0.25)[0][20]).max() == 0.0
+
+
+# ---------------------------------------------------------------- P7: hand counts
+def test_visible_pairs_hand_count_tiny_trace():
+    gold = json.load(open(os.path.join(GOLDEN, "trace512_tiny_visible_pairs.json")))
+    wl = inputs.WORKLOADS["trace512_tiny"]
+    e = wl.evict_at()
+    assert orc.visible_pairs(e, wl.lengths) == gold["total"]
+    assert sum(sp["pairs"] for sp in gold["spans"]) == gold["total"]
+    c = tiles.tile_counts(e, 512, 64, 64)
+    assert c.sum() == gold["total"]
+
+
+@pytest.mark.parametrize("BM,BN", [(64, 64), (32, 64), (128, 128), (16, 48)])
+def test_tile_classes_account_for_every_visible_pair(BM, BN):
+    rng = np.random.default_rng(BM + BN)
+    for L in (1, 7, 129, 300):
+        e = inputs.evict_at_random(L, rng)
+        c = tiles.tile_counts(e, L, BM, BN)
+        cls = tiles.tile_classes(e, L, BM, BN)
+        assert c.sum() == orc.visible_pairs(e, [L])
+        assert (cls == tiles.FULL).sum() * BM * BN + c[cls == tiles.PARTIAL].sum() == c.sum()
+        assert np.all(c[cls == tiles.EMPTY] == 0)
+
+
+def test_tile_classes_small_worked_case():
+    # 8 tokens, 4x4 tiles; key 0 never evicted, keys 1..3 evicted at 4, keys 4..7 never.
+    e = np.array([8, 4, 4, 4, 8, 8, 8, 8])
+    cls = tiles.tile_classes(e, 8, 4, 4)
+    # tile (0,0): lower triangle of rows 0..3 -> partial; (0,1) above diagonal -> empty;
+    # (1,0): rows 4..7 see only key 0 -> partial; (1,1): lower triangle -> partial
+    assert cls.tolist() == [[1, 0], [1, 1]]
+    e2 = np.array([8, 8, 8, 8, 8, 8, 8, 8])
+    assert tiles.tile_classes(e2, 8, 4, 4).tolist() == [[1, 0], [2, 1]]
+    e3 = np.array([1, 2, 3, 4, 8, 8, 8, 8])
+    assert tiles.tile_classes(e3, 8, 4, 4).tolist() == [[1, 0], [0, 1]]
+
+
+# ---------------------------------------------------------------- P8: packed traces are independent
+def test_varlen_is_concatenation():
+    lengths = [13, 1, 40, 0, 27]
+    Hq, Hkv, D = 4, 2, 8
+    n = sum(lengths)
+    rng = np.random.default_rng(3)
+    e = np.concatenate([inputs.evict_at_random(L, rng) for L in lengths if L] + [np.zeros(0, dtype=np.int32)])
+    q, k, v, do = _rand((n, Hq, D), 61), _rand((n, Hkv, D), 62), _rand((n, Hkv, D), 63), _rand((n, Hq, D), 64)
+    cu = np.concatenate([[0], np.cumsum(lengths)])
+    res = orc.backward(q, k, v, e, 0.3, do, cu_seqlens=cu)
+    for b in range(len(lengths)):
+        a, z = cu[b], cu[b + 1]
+        if a == z:
+            continue
+        one = orc.backward(q[a:z], k[a:z], v[a:z], e[a:z], 0.3, do[a:z])
+        for key in ("O", "dq", "dk", "dv"):
+            np.testing.assert_array_equal(res[key][a:z], one[key])
+        np.testing.assert_array_equal(res["LSE"][:, a:z], one["LSE"])
+
+
+def test_invalid_evict_at_rejected():
+    q = _rand((5, 1, 8), 1)
+    with pytest.raises(ValueError):
+        orc.forward(q, q, q, np.array([1, 2, 2, 5, 5]), 1.0)
