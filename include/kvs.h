@@ -1,0 +1,167 @@
+/*
+ * kvs.h -- C ABI of the eviction-masked attention library (libkvs.so) for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * What it computes.  KV-streams (Section 2, paragraph "KV-streams") keeps the
+ * retained keys and values of a compacted agent trace at their original
+ * positions and reproduces each compaction in the trainer with an attention
+ * mask over one continuous trace, in a single forward pass.  The engine
+ * drops evicted entries for good (Section 7, second paragraph), so every key
+ * token j of a trace carries one eviction index evict_at[j], and query i
+ * attends to key j iff
+ *
+ *        j <= i < evict_at[j]      (evict_at[j] >= L, e.g. INT32_MAX, = never evicted)
+ *
+ * For q-head h of KV head g = h / (Hq / Hkv) (contiguous GQA groups):
+ *        s_ij  = softmax_scale * <Q_i^h, K_j^g>
+ *        LSE_i = ln sum_{visible j} exp(s_ij)
+ *        O_i   = sum_{visible j} exp(s_ij - LSE_i) V_j^g
+ * and the backward gives dQ, dK, dV of sum(dO * O) (dK, dV summed over the
+ * q-heads of each group).  Every query sees at least itself (evict_at[j] > j
+ * is required), so no row is empty.
+ *
+ * Conventions shared by every entry point:
+ *  - Tensor pointers are DEVICE pointers owned by the caller; the library
+ *    never allocates device memory and keeps no per-call state.  Scratch space
+ *    comes from the caller's workspace (size from the *_workspace query; any
+ *    256-byte aligned device buffer of at least that size).
+ *  - bf16 tensors are row-major with D innermost:
+ *       fixed length:  Q, O, dO, dQ [B][T][Hq][D];  K, V, dK, dV [B][T][Hkv][D]
+ *       varlen:        Q, O, dO, dQ [Ntot][Hq][D];  K, V, dK, dV [Ntot][Hkv][D]
+ *    LSE is fp32, natural log: fixed [B][Hq][T], varlen [Hq][Ntot].
+ *    evict_at is int32: fixed [B][T], varlen [Ntot]; values are trace-local
+ *    token indices.  Tensor pointers must be 16-byte aligned.
+ *  - cu_seqlens (varlen) is a device int32 array [B+1]: cu[0] = 0,
+ *    cu[B] = Ntot, non-decreasing; trace b is tokens [cu[b], cu[b+1]).
+ *    No attention crosses traces.  max_seqlen must be >= every trace length.
+ *  - `stream` is a hipStream_t (NULL = the null stream).  Calls only enqueue
+ *    work on it and return; none synchronizes except kvs_check_evict_at.
+ *  - Outputs are overwritten, never accumulated.
+ *  - Supported: D in {64, 128}; 1 <= Hkv <= Hq, Hq % Hkv == 0, Hq / Hkv <= 64;
+ *    T (max_seqlen) <= 1048576.  Other shapes return KVS_ERR_SHAPE or
+ *    KVS_ERR_UNSUPPORTED.
+ *  - Arguments are validated on the host before any HIP call, so invalid
+ *    calls fail the same way on machines without a GPU.
+ *  - Results are unspecified if some evict_at[j] <= j (trace-local); use
+ *    kvs_check_evict_at to detect that.
+ */
+#ifndef KVS_H_
+#define KVS_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define KVS_ABI_VERSION 1
+
+typedef enum {
+  KVS_OK = 0,
+  KVS_ERR_NULL = 1,         /* a required pointer is NULL */
+  KVS_ERR_SHAPE = 2,        /* bad sizes: B,T,Hq,Hkv < 1, Hq % Hkv != 0, D not 64/128, bad BM/BN */
+  KVS_ERR_ALIGN = 3,        /* a tensor pointer is not 16-byte aligned (workspace: 256-byte) */
+  KVS_ERR_WORKSPACE = 4,    /* workspace smaller than the *_workspace query */
+  KVS_ERR_EVICT = 5,        /* invalid evict_at (only kvs_check_evict_at reports it) */
+  KVS_ERR_HIP = 6,          /* a HIP launch or runtime call failed; see kvs_last_error() */
+  KVS_ERR_UNSUPPORTED = 7   /* valid but outside the supported limits above */
+} kvs_status_t;
+
+/* ABI version of the loaded library (KVS_ABI_VERSION it was built with). */
+int kvs_abi_version(void);
+
+/* Static English text for a status code; never NULL. */
+const char* kvs_status_string(kvs_status_t status);
+
+/* Detail of the most recent failure on the calling thread (which argument,
+ * which HIP error); "" if none.  Valid until the next call on that thread. */
+const char* kvs_last_error(void);
+
+/* ---------------------------------------------------------------- forward
+ * Eviction-masked attention forward (Section 2, "KV-streams": one pass over
+ * the continuous trace with a mask that blocks each deleted span).
+ * Writes O (bf16) and LSE (fp32, natural log).  B traces of equal length T.
+ */
+size_t kvs_evict_attn_fwd_workspace(int B, int T, int Hq, int Hkv, int D);
+kvs_status_t kvs_evict_attn_fwd(const void* Q, const void* K, const void* V,
+                                const int32_t* evict_at,
+                                void* O, float* LSE,
+                                int B, int T, int Hq, int Hkv, int D, float softmax_scale,
+                                void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------- backward
+ * Gradients of sum(dO * O) for the forward above: dQ, dK, dV (bf16, shapes
+ * of Q, K, V).  O and LSE must be the forward's outputs for the same inputs.
+ */
+size_t kvs_evict_attn_bwd_workspace(int B, int T, int Hq, int Hkv, int D);
+kvs_status_t kvs_evict_attn_bwd(const void* dO, const void* Q, const void* K, const void* V,
+                                const void* O, const float* LSE, const int32_t* evict_at,
+                                void* dQ, void* dK, void* dV,
+                                int B, int T, int Hq, int Hkv, int D, float softmax_scale,
+                                void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------- varlen
+ * The same computations over B traces packed back to back (several rollouts
+ * in one batch, each its own continuous trace; Section 2).  Layouts as above
+ * with the varlen shapes; evict_at values are local to each trace.
+ */
+size_t kvs_evict_attn_varlen_fwd_workspace(int B, int Ntot, int max_seqlen, int Hq, int Hkv, int D);
+kvs_status_t kvs_evict_attn_varlen_fwd(const void* Q, const void* K, const void* V,
+                                       const int32_t* evict_at, const int32_t* cu_seqlens,
+                                       void* O, float* LSE,
+                                       int B, int Ntot, int max_seqlen, int Hq, int Hkv, int D,
+                                       float softmax_scale,
+                                       void* workspace, size_t workspace_bytes, void* stream);
+size_t kvs_evict_attn_varlen_bwd_workspace(int B, int Ntot, int max_seqlen, int Hq, int Hkv, int D);
+kvs_status_t kvs_evict_attn_varlen_bwd(const void* dO, const void* Q, const void* K, const void* V,
+                                       const void* O, const float* LSE,
+                                       const int32_t* evict_at, const int32_t* cu_seqlens,
+                                       void* dQ, void* dK, void* dV,
+                                       int B, int Ntot, int max_seqlen, int Hq, int Hkv, int D,
+                                       float softmax_scale,
+                                       void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------- tile classes
+ * Class of every BM x BN tile of the mask: 0 = EMPTY (no visible element,
+ * skipped), 1 = PARTIAL (per-element mask), 2 = FULL (every element
+ * visible).  Tiles start at each trace's first token; elements outside the
+ * trace count as masked.  Output: per-trace grids, each row-major
+ * [ceil(L_b/BM)][ceil(L_b/BN)], concatenated in trace order into tile_class
+ * (device uint8, caller-sized).  cu_seqlens NULL means B traces of length T;
+ * otherwise T is Ntot.  The attention kernels classify with the same rule
+ * (BM multiple of 16 in [16, 256], BN in {32, 64, 128}).
+ */
+kvs_status_t kvs_classify_tiles(const int32_t* evict_at, const int32_t* cu_seqlens, int B, int T,
+                                int BM, int BN, uint8_t* tile_class, void* stream);
+
+/* Number of bytes kvs_classify_tiles writes when the trace lengths are known
+ * on the host (lengths: host int32 [B]). */
+size_t kvs_classify_tiles_size(const int32_t* lengths, int B, int BM, int BN);
+
+/* ---------------------------------------------------------------- validation
+ * Synchronous check that every key is visible to itself (evict_at[j] > j,
+ * trace-local).  On return *first_bad (host) is the packed index of the first
+ * offending key, or -1.  Returns KVS_ERR_EVICT if one exists.  cu_seqlens as
+ * in kvs_classify_tiles.  Blocks until the stream reaches it.
+ */
+kvs_status_t kvs_check_evict_at(const int32_t* evict_at, const int32_t* cu_seqlens, int B, int T,
+                                int64_t* first_bad, void* stream);
+
+/* ---------------------------------------------------------------- timing
+ * Per-kernel timing for benchmarks.  While enabled, each call brackets every
+ * kernel it launches with HIP events on the call's stream.  kvs_prof_read
+ * waits for the recorded events and returns, for the kernel named `name`
+ * ("classify", "fwd", "bwd_pre", "bwd_dkdv", "bwd_dq"), the number of
+ * launches and their total duration in milliseconds.  Not thread-safe;
+ * meant for single-threaded benchmark drivers.
+ */
+void kvs_prof_enable(int on);
+void kvs_prof_reset(void);
+kvs_status_t kvs_prof_read(const char* name, int* launches, double* total_ms);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVS_H_ */

@@ -1,0 +1,341 @@
+// C ABI of libkvs: argument validation, workspace layout and launch order.
+// Validation runs before any HIP call, so invalid calls fail identically on
+// machines without a GPU.
+#include "kvs.h"
+
+#include <hip/hip_runtime_api.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "kvs_launch.h"
+
+namespace {
+
+thread_local std::string t_err;
+
+kvs_status_t fail(kvs_status_t st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  t_err = buf;
+  return st;
+}
+
+kvs_status_t hip_fail(hipError_t e, const char* where) {
+  return fail(KVS_ERR_HIP, "%s: %s (%d)", where, hipGetErrorString(e), (int)e);
+}
+
+constexpr int kMaxSeq = 1 << 20;
+constexpr int kMaxGroup = 64;
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+// Shape rules shared by every attention entry point.
+kvs_status_t check_dims(int B, int T, long long ntok, int Hq, int Hkv, int D) {
+  if (B < 1 || T < 1 || Hq < 1 || Hkv < 1)
+    return fail(KVS_ERR_SHAPE, "B, T (max_seqlen), Hq, Hkv must be >= 1 (got %d, %d, %d, %d)", B, T, Hq, Hkv);
+  if (Hq % Hkv != 0) return fail(KVS_ERR_SHAPE, "Hq (%d) must be a multiple of Hkv (%d)", Hq, Hkv);
+  if (D != 64 && D != 128) return fail(KVS_ERR_SHAPE, "head dim D must be 64 or 128 (got %d)", D);
+  if (ntok < 0) return fail(KVS_ERR_SHAPE, "Ntot must be >= 0");
+  if (T > kMaxSeq) return fail(KVS_ERR_UNSUPPORTED, "sequence length %d above the supported %d", T, kMaxSeq);
+  if (Hq / Hkv > kMaxGroup) return fail(KVS_ERR_UNSUPPORTED, "GQA group size %d above %d", Hq / Hkv, kMaxGroup);
+  if (ntok * (long long)Hq * D >= (1ll << 40))
+    return fail(KVS_ERR_UNSUPPORTED, "tensor of %lld elements too large", ntok * (long long)Hq * D);
+  if (ntok > 0x7fffffffll) return fail(KVS_ERR_UNSUPPORTED, "Ntot above INT32_MAX");
+  return KVS_OK;
+}
+
+// Workgroup shape of the row kernels: HG q-heads (largest divisor of G that
+// is <= 8) times TC chunks of 32 tokens, 4 to 8 waves in all.
+void head_grouping(kvs::Problem& p) {
+  int hg = 1;
+  for (int d = 1; d <= 8; ++d)
+    if (p.G % d == 0) hg = d;
+  p.HG = hg;
+  p.TC = hg >= 4 ? 1 : (hg == 3 ? 2 : 4 / hg);
+  p.nhg = p.G / hg;
+}
+
+size_t fwd_ws(int B, long long ntok) { return kvs::ws_kstats_bytes(B, (int)ntok); }
+size_t bwd_ws(int B, long long ntok, int Hq) {
+  return kvs::ws_kstats_bytes(B, (int)ntok) + kvs::ws_delta_bytes(Hq, (int)ntok);
+}
+
+kvs_status_t check_ws(void* ws, size_t have, size_t need) {
+  if (need == 0) return KVS_OK;
+  if (!ws) return fail(KVS_ERR_NULL, "workspace is NULL (%zu bytes needed)", need);
+  if (((uintptr_t)ws & 255u) != 0) return fail(KVS_ERR_ALIGN, "workspace must be 256-byte aligned");
+  if (have < need) return fail(KVS_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", have, need);
+  return KVS_OK;
+}
+
+#define REQUIRE_PTR(p, name)                                         \
+  do {                                                               \
+    if (!(p)) return fail(KVS_ERR_NULL, "%s is NULL", name);         \
+    if (!aligned16(p)) return fail(KVS_ERR_ALIGN, "%s not 16-byte aligned", name); \
+  } while (0)
+
+kvs_status_t run_fwd(kvs::Problem& p) {
+  head_grouping(p);
+  int2* kstats = (int2*)p.ws;
+  hipError_t e = kvs::launch_kstats(p, 64, kstats);
+  if (e != hipSuccess) return hip_fail(e, "key-tile statistics launch");
+  e = kvs::launch_fwd(p, kstats);
+  if (e != hipSuccess) return hip_fail(e, "forward launch");
+  return KVS_OK;
+}
+
+kvs_status_t run_bwd(kvs::Problem& p) {
+  head_grouping(p);
+  int2* kstats = (int2*)p.ws;
+  float* delta = (float*)((char*)p.ws + kvs::ws_kstats_bytes(p.B, p.ntok));
+  hipError_t e = kvs::launch_kstats(p, 64, kstats);
+  if (e != hipSuccess) return hip_fail(e, "key-tile statistics launch");
+  e = kvs::launch_bwd_pre(p, delta);
+  if (e != hipSuccess) return hip_fail(e, "backward preprocess launch");
+  e = kvs::launch_bwd_dkdv(p, delta);
+  if (e != hipSuccess) return hip_fail(e, "dK/dV launch");
+  e = kvs::launch_bwd_dq(p, kstats, delta);
+  if (e != hipSuccess) return hip_fail(e, "dQ launch");
+  return KVS_OK;
+}
+
+// ---------------------------------------------------------------- timing records
+struct ProfRec {
+  const char* name;
+  hipEvent_t a, b;
+};
+bool g_prof = false;
+std::vector<ProfRec> g_recs;
+const char* g_pending = nullptr;
+hipEvent_t g_pending_ev = nullptr;
+
+}  // namespace
+
+namespace kvs {
+void prof_begin(const char* name, hipStream_t s) {
+  if (!g_prof) return;
+  hipEvent_t ev;
+  if (hipEventCreate(&ev) != hipSuccess) return;
+  (void)hipEventRecord(ev, s);
+  g_pending = name;
+  g_pending_ev = ev;
+}
+void prof_end(hipStream_t s) {
+  if (!g_prof || !g_pending_ev) return;
+  hipEvent_t ev;
+  if (hipEventCreate(&ev) != hipSuccess) return;
+  (void)hipEventRecord(ev, s);
+  g_recs.push_back({g_pending, g_pending_ev, ev});
+  g_pending_ev = nullptr;
+}
+}  // namespace kvs
+
+extern "C" {
+
+int kvs_abi_version(void) { return KVS_ABI_VERSION; }
+
+const char* kvs_status_string(kvs_status_t s) {
+  switch (s) {
+    case KVS_OK: return "ok";
+    case KVS_ERR_NULL: return "null pointer";
+    case KVS_ERR_SHAPE: return "invalid shape";
+    case KVS_ERR_ALIGN: return "misaligned pointer";
+    case KVS_ERR_WORKSPACE: return "workspace too small";
+    case KVS_ERR_EVICT: return "invalid evict_at (some evict_at[j] <= j)";
+    case KVS_ERR_HIP: return "HIP runtime error";
+    case KVS_ERR_UNSUPPORTED: return "unsupported configuration";
+  }
+  return "unknown status";
+}
+
+const char* kvs_last_error(void) { return t_err.c_str(); }
+
+size_t kvs_evict_attn_fwd_workspace(int B, int T, int Hq, int Hkv, int D) {
+  if (B < 1 || T < 1) return 0;
+  (void)Hq; (void)Hkv; (void)D;
+  return fwd_ws(B, (long long)B * T);
+}
+
+size_t kvs_evict_attn_bwd_workspace(int B, int T, int Hq, int Hkv, int D) {
+  if (B < 1 || T < 1 || Hq < 1) return 0;
+  (void)Hkv; (void)D;
+  return bwd_ws(B, (long long)B * T, Hq);
+}
+
+size_t kvs_evict_attn_varlen_fwd_workspace(int B, int Ntot, int max_seqlen, int Hq, int Hkv, int D) {
+  if (B < 1 || Ntot < 0) return 0;
+  (void)max_seqlen; (void)Hq; (void)Hkv; (void)D;
+  return fwd_ws(B, Ntot);
+}
+
+size_t kvs_evict_attn_varlen_bwd_workspace(int B, int Ntot, int max_seqlen, int Hq, int Hkv, int D) {
+  if (B < 1 || Ntot < 0 || Hq < 1) return 0;
+  (void)max_seqlen; (void)Hkv; (void)D;
+  return bwd_ws(B, Ntot, Hq);
+}
+
+static kvs_status_t fwd_common(const void* Q, const void* K, const void* V, const int32_t* evict_at,
+                               const int32_t* cu, void* O, float* LSE, int B, int T, long long ntok, int Hq,
+                               int Hkv, int D, float scale, void* ws, size_t ws_bytes, void* stream) {
+  t_err.clear();
+  kvs_status_t st = check_dims(B, T, ntok, Hq, Hkv, D);
+  if (st != KVS_OK) return st;
+  REQUIRE_PTR(Q, "Q");
+  REQUIRE_PTR(K, "K");
+  REQUIRE_PTR(V, "V");
+  REQUIRE_PTR(O, "O");
+  REQUIRE_PTR(LSE, "LSE");
+  if (!evict_at) return fail(KVS_ERR_NULL, "evict_at is NULL");
+  if (!(scale > 0.f) || scale != scale) return fail(KVS_ERR_SHAPE, "softmax_scale must be positive and finite");
+  st = check_ws(ws, ws_bytes, fwd_ws(B, ntok));
+  if (st != KVS_OK) return st;
+  if (ntok == 0) return KVS_OK;
+  kvs::Problem p{};
+  p.q = Q; p.k = K; p.v = V; p.evict = evict_at; p.cu = cu; p.o = O; p.lse = LSE;
+  p.B = B; p.T = T; p.ntok = (int)ntok; p.Hq = Hq; p.Hkv = Hkv; p.D = D; p.G = Hq / Hkv;
+  p.scale = scale; p.ws = ws; p.stream = (hipStream_t)stream;
+  return run_fwd(p);
+}
+
+static kvs_status_t bwd_common(const void* dO, const void* Q, const void* K, const void* V, const void* O,
+                               const float* LSE, const int32_t* evict_at, const int32_t* cu, void* dQ, void* dK,
+                               void* dV, int B, int T, long long ntok, int Hq, int Hkv, int D, float scale, void* ws,
+                               size_t ws_bytes, void* stream) {
+  t_err.clear();
+  kvs_status_t st = check_dims(B, T, ntok, Hq, Hkv, D);
+  if (st != KVS_OK) return st;
+  REQUIRE_PTR(dO, "dO");
+  REQUIRE_PTR(Q, "Q");
+  REQUIRE_PTR(K, "K");
+  REQUIRE_PTR(V, "V");
+  REQUIRE_PTR(O, "O");
+  REQUIRE_PTR(LSE, "LSE");
+  REQUIRE_PTR(dQ, "dQ");
+  REQUIRE_PTR(dK, "dK");
+  REQUIRE_PTR(dV, "dV");
+  if (!evict_at) return fail(KVS_ERR_NULL, "evict_at is NULL");
+  if (!(scale > 0.f) || scale != scale) return fail(KVS_ERR_SHAPE, "softmax_scale must be positive and finite");
+  st = check_ws(ws, ws_bytes, bwd_ws(B, ntok, Hq));
+  if (st != KVS_OK) return st;
+  if (ntok == 0) return KVS_OK;
+  kvs::Problem p{};
+  p.q = Q; p.k = K; p.v = V; p.o_in = O; p.dout = dO; p.lse_in = LSE; p.evict = evict_at; p.cu = cu;
+  p.dq = dQ; p.dk = dK; p.dv = dV;
+  p.B = B; p.T = T; p.ntok = (int)ntok; p.Hq = Hq; p.Hkv = Hkv; p.D = D; p.G = Hq / Hkv;
+  p.scale = scale; p.ws = ws; p.stream = (hipStream_t)stream;
+  return run_bwd(p);
+}
+
+kvs_status_t kvs_evict_attn_fwd(const void* Q, const void* K, const void* V, const int32_t* evict_at, void* O,
+                                float* LSE, int B, int T, int Hq, int Hkv, int D, float softmax_scale,
+                                void* workspace, size_t workspace_bytes, void* stream) {
+  return fwd_common(Q, K, V, evict_at, nullptr, O, LSE, B, T, (long long)B * T, Hq, Hkv, D, softmax_scale,
+                    workspace, workspace_bytes, stream);
+}
+
+kvs_status_t kvs_evict_attn_bwd(const void* dO, const void* Q, const void* K, const void* V, const void* O,
+                                const float* LSE, const int32_t* evict_at, void* dQ, void* dK, void* dV, int B,
+                                int T, int Hq, int Hkv, int D, float softmax_scale, void* workspace,
+                                size_t workspace_bytes, void* stream) {
+  return bwd_common(dO, Q, K, V, O, LSE, evict_at, nullptr, dQ, dK, dV, B, T, (long long)B * T, Hq, Hkv, D,
+                    softmax_scale, workspace, workspace_bytes, stream);
+}
+
+kvs_status_t kvs_evict_attn_varlen_fwd(const void* Q, const void* K, const void* V, const int32_t* evict_at,
+                                       const int32_t* cu_seqlens, void* O, float* LSE, int B, int Ntot,
+                                       int max_seqlen, int Hq, int Hkv, int D, float softmax_scale, void* workspace,
+                                       size_t workspace_bytes, void* stream) {
+  if (!cu_seqlens) return fail(KVS_ERR_NULL, "cu_seqlens is NULL");
+  return fwd_common(Q, K, V, evict_at, cu_seqlens, O, LSE, B, max_seqlen, Ntot, Hq, Hkv, D, softmax_scale,
+                    workspace, workspace_bytes, stream);
+}
+
+kvs_status_t kvs_evict_attn_varlen_bwd(const void* dO, const void* Q, const void* K, const void* V, const void* O,
+                                       const float* LSE, const int32_t* evict_at, const int32_t* cu_seqlens,
+                                       void* dQ, void* dK, void* dV, int B, int Ntot, int max_seqlen, int Hq,
+                                       int Hkv, int D, float softmax_scale, void* workspace, size_t workspace_bytes,
+                                       void* stream) {
+  if (!cu_seqlens) return fail(KVS_ERR_NULL, "cu_seqlens is NULL");
+  return bwd_common(dO, Q, K, V, O, LSE, evict_at, cu_seqlens, dQ, dK, dV, B, max_seqlen, Ntot, Hq, Hkv, D,
+                    softmax_scale, workspace, workspace_bytes, stream);
+}
+
+kvs_status_t kvs_classify_tiles(const int32_t* evict_at, const int32_t* cu_seqlens, int B, int T, int BM, int BN,
+                                uint8_t* tile_class, void* stream) {
+  t_err.clear();
+  if (B < 1 || T < 1) return fail(KVS_ERR_SHAPE, "B and T must be >= 1");
+  if (T > kMaxSeq * 16) return fail(KVS_ERR_UNSUPPORTED, "T above %d", kMaxSeq * 16);
+  if (BM < 16 || BM > 256 || BM % 16 != 0) return fail(KVS_ERR_SHAPE, "BM must be a multiple of 16 in [16, 256]");
+  if (BN != 32 && BN != 64 && BN != 128) return fail(KVS_ERR_SHAPE, "BN must be 32, 64 or 128");
+  if (!evict_at) return fail(KVS_ERR_NULL, "evict_at is NULL");
+  if (!tile_class) return fail(KVS_ERR_NULL, "tile_class is NULL");
+  hipError_t e = kvs::launch_classify(evict_at, cu_seqlens, B, T, BM, BN, tile_class, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "classify launch");
+  return KVS_OK;
+}
+
+size_t kvs_classify_tiles_size(const int32_t* lengths, int B, int BM, int BN) {
+  if (!lengths || B < 1 || BM < 1 || BN < 1) return 0;
+  size_t n = 0;
+  for (int b = 0; b < B; ++b) {
+    const long long L = lengths[b] > 0 ? lengths[b] : 0;
+    n += (size_t)((L + BM - 1) / BM) * (size_t)((L + BN - 1) / BN);
+  }
+  return n;
+}
+
+kvs_status_t kvs_check_evict_at(const int32_t* evict_at, const int32_t* cu_seqlens, int B, int T,
+                                int64_t* first_bad, void* stream) {
+  t_err.clear();
+  if (!first_bad) return fail(KVS_ERR_NULL, "first_bad is NULL");
+  *first_bad = -1;
+  if (B < 1 || T < 0) return fail(KVS_ERR_SHAPE, "B must be >= 1 and T >= 0");
+  if (!evict_at) return fail(KVS_ERR_NULL, "evict_at is NULL");
+  const long long ntok = cu_seqlens ? T : (long long)B * T;
+  if (ntok > 0x7fffffffll) return fail(KVS_ERR_UNSUPPORTED, "too many tokens");
+  int cu_bad = 0;
+  hipError_t e = kvs::launch_check(evict_at, cu_seqlens, B, T, (int)ntok, first_bad, &cu_bad, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "evict_at check");
+  if (cu_bad) return fail(KVS_ERR_SHAPE, "cu_seqlens is not 0 = cu[0] <= ... <= cu[B] = Ntot");
+  if (*first_bad >= 0) return fail(KVS_ERR_EVICT, "evict_at[%lld] <= its local index", (long long)*first_bad);
+  return KVS_OK;
+}
+
+void kvs_prof_enable(int on) { g_prof = on != 0; }
+
+void kvs_prof_reset(void) {
+  for (auto& r : g_recs) {
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  g_recs.clear();
+}
+
+kvs_status_t kvs_prof_read(const char* name, int* launches, double* total_ms) {
+  t_err.clear();
+  if (!name || !launches || !total_ms) return fail(KVS_ERR_NULL, "NULL argument");
+  int n = 0;
+  double tot = 0.0;
+  for (auto& r : g_recs) {
+    if (std::strcmp(r.name, name) != 0) continue;
+    hipError_t e = hipEventSynchronize(r.b);
+    if (e != hipSuccess) return hip_fail(e, "event synchronize");
+    float ms = 0.f;
+    e = hipEventElapsedTime(&ms, r.a, r.b);
+    if (e != hipSuccess) return hip_fail(e, "event elapsed time");
+    ++n;
+    tot += ms;
+  }
+  *launches = n;
+  *total_ms = tot;
+  return KVS_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,54 @@
+// Internal interface between the C ABI layer (kvs_api.cpp) and the kernel
+// launchers (kvs_kernels.hip).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+
+namespace kvs {
+
+// Problem description after host-side validation.
+struct Problem {
+  const void* q;
+  const void* k;
+  const void* v;
+  const void* o_in;      // backward: forward output O
+  const void* dout;      // backward: dO
+  const float* lse_in;   // backward: forward LSE
+  const int32_t* evict;
+  const int32_t* cu;     // NULL: fixed length
+  void* o;               // forward output
+  float* lse;            // forward output
+  void* dq;
+  void* dk;
+  void* dv;
+  int B;
+  int T;        // fixed: trace length; varlen: max_seqlen
+  int ntok;     // total packed tokens
+  int Hq, Hkv, D, G;
+  int HG, TC, nhg;   // q-heads per workgroup, 32-token chunks per workgroup, head groups per KV head
+  float scale;
+  void* ws;
+  hipStream_t stream;
+};
+
+// Workspace pieces (byte offsets from the workspace start).
+size_t ws_kstats_bytes(int B, int ntok);
+size_t ws_delta_bytes(int Hq, int ntok);
+
+// Launchers.  Each returns the hipError_t of its launch(es).
+hipError_t launch_kstats(const Problem& p, int BN, int2* kstats);
+hipError_t launch_fwd(const Problem& p, const int2* kstats);
+hipError_t launch_bwd_pre(const Problem& p, float* delta);
+hipError_t launch_bwd_dkdv(const Problem& p, const float* delta);
+hipError_t launch_bwd_dq(const Problem& p, const int2* kstats, const float* delta);
+hipError_t launch_classify(const int32_t* evict, const int32_t* cu, int B, int T, int BM, int BN,
+                           uint8_t* out, hipStream_t stream);
+hipError_t launch_check(const int32_t* evict, const int32_t* cu, int B, int T, int ntok,
+                        int64_t* first_bad, int* cu_bad, hipStream_t stream);
+
+// Per-kernel event bracketing (benchmark timing).
+void prof_begin(const char* name, hipStream_t s);
+void prof_end(hipStream_t s);
+
+}  // namespace kvs

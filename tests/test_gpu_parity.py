@@ -1,0 +1,164 @@
+"""HIP path vs the fp64 checker, element by element, on seeded inputs (MI355X).
+
+Sizes here are ones the checker finishes in seconds while still spanning
+several tiles and ragged tails.  Every case prints its name before it runs.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import attention as orc
+from oracle import tiles as otiles
+from paper_2609_35750_amd import inputs
+from tests.gpu_helpers import LSE_ABS, MAX_ABS, announce, assert_close, gpu_fwd_bwd, scaled_max_abs, to_f64
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def kvs():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_35750_amd import kvs as k
+
+    return k
+
+
+def _parity(kvs, wl, e, cu=None, B=None, scaled=True):
+    t = inputs.make_tensors(wl)
+    scale = wl.softmax_scale
+    announce(f"{wl.name} lengths={wl.lengths} Hq={wl.Hq} Hkv={wl.Hkv} D={wl.D} varlen={cu is not None} B={B}")
+    res = gpu_fwd_bwd(kvs, t["q"], t["k"], t["v"], t["do"], e, scale, cu_seqlens=cu,
+                      max_seqlen=max(wl.lengths) if cu is not None else None, B=B)
+    ref = orc.backward(t["q"], t["k"], t["v"], e, scale, t["do"],
+                       cu_seqlens=cu if cu is not None else (np.arange(B + 1) * wl.lengths[0] if B else None))
+    out = {}
+    for key, rkey in (("O", "O"), ("dq", "dq"), ("dk", "dk"), ("dv", "dv")):
+        bound = scaled_max_abs(ref[rkey]) if scaled else MAX_ABS
+        out[key] = assert_close(f"{wl.name}:{key}", to_f64(res[key]), ref[rkey], max_abs=bound)
+    assert_close(f"{wl.name}:LSE", to_f64(res["LSE"]), ref["LSE"], max_abs=LSE_ABS, rel_l2=1e-4)
+    return out
+
+
+def test_tiny_trace_all_outputs(kvs):
+    wl = inputs.WORKLOADS["trace512_tiny"]
+    _parity(kvs, wl, wl.evict_at(), scaled=False)
+
+
+LAYOUT_CASES = [
+    # (L, Hq, Hkv, D, p, w, s, strategy)
+    (1, 2, 2, 64, 0, 1, 0, "keep_all"),
+    (17, 4, 4, 128, 3, 5, 2, "keep_all"),
+    (100, 8, 2, 128, 10, 30, 7, "latest_only"),
+    (257, 5, 1, 128, 16, 48, 16, "last2"),
+    (300, 8, 1, 64, 20, 64, 16, "keep_all"),
+    (641, 6, 2, 128, 64, 128, 32, "last2"),
+    (700, 3, 3, 64, 33, 97, 13, "latest_only"),
+    (1024, 16, 2, 128, 64, 200, 40, "keep_all"),
+]
+
+
+@pytest.mark.parametrize("case", LAYOUT_CASES, ids=lambda c: f"L{c[0]}_H{c[1]}x{c[2]}_D{c[3]}_{c[7]}")
+def test_layouts(kvs, case):
+    L, Hq, Hkv, D, p, w, s, strat = case
+    wl = inputs.custom_workload(f"layout_L{L}", Hq, Hkv, D, [L], p, w, s, strat, seed=L)
+    _parity(kvs, wl, wl.evict_at())
+
+
+@pytest.mark.parametrize("L,Hq,Hkv,D,seed", [(130, 4, 2, 128, 1), (333, 2, 1, 64, 2), (515, 10, 2, 128, 3)])
+def test_random_evict_at(kvs, L, Hq, Hkv, D, seed):
+    wl = inputs.custom_workload(f"random_L{L}", Hq, Hkv, D, [L], 0, 1, 0, seed=seed + 50)
+    e = inputs.evict_at_random(L, np.random.default_rng(seed))
+    _parity(kvs, wl, e)
+
+
+def test_fixed_batch_of_traces(kvs):
+    wl = inputs.custom_workload("batch3", 4, 2, 128, [200, 200, 200], 8, 40, 8, "latest_only", varlen=False, seed=9)
+    _parity(kvs, wl, wl.evict_at(), B=3)
+
+
+def test_varlen_ragged(kvs):
+    wl = inputs.custom_workload("varlen_small", 10, 2, 128, [37, 1, 300, 129, 64], 4, 50, 10, "keep_all",
+                                varlen=True, seed=13)
+    _parity(kvs, wl, wl.evict_at(), cu=wl.cu_seqlens())
+
+
+def test_self_only_closed_form(kvs):
+    # every key lives for one query: O_i = v_i, dQ = dK = 0, dV_j = sum over the group of dO_j
+    L, Hq, Hkv, D = 200, 4, 2, 128
+    wl = inputs.custom_workload("self_only", Hq, Hkv, D, [L], 0, 1, 0, seed=77)
+    t = inputs.make_tensors(wl)
+    e = np.arange(1, L + 1, dtype=np.int32)
+    announce("self_only closed form")
+    res = gpu_fwd_bwd(kvs, t["q"], t["k"], t["v"], t["do"], e, 0.1)
+    v = t["v"].double().numpy()
+    G = Hq // Hkv
+    for h in range(Hq):
+        assert_close("O", to_f64(res["O"][:, h]), v[:, h // G], max_abs=1e-6, rel_l2=1e-6)
+    # dS = P (dP - Delta) vanishes up to the fp32 rounding of two sums of the same products
+    assert float(res["dq"].abs().max()) < 1e-4 and float(res["dk"].abs().max()) < 1e-4
+    ref_dv = t["do"].double().numpy().reshape(L, Hkv, G, D).sum(2)
+    assert_close("dV", to_f64(res["dv"]), ref_dv, max_abs=2e-2, rel_l2=5e-3)
+
+
+def test_forward_is_deterministic(kvs):
+    wl = inputs.custom_workload("det", 8, 2, 128, [900], 64, 200, 50, "last2", seed=21)
+    t = inputs.make_tensors(wl)
+    announce("determinism")
+    a = gpu_fwd_bwd(kvs, t["q"], t["k"], t["v"], t["do"], wl.evict_at(), wl.softmax_scale)
+    b = gpu_fwd_bwd(kvs, t["q"], t["k"], t["v"], t["do"], wl.evict_at(), wl.softmax_scale)
+    for key in ("O", "LSE", "dq", "dk", "dv"):
+        assert torch.equal(a[key], b[key]), key
+
+
+@pytest.mark.parametrize("BM,BN", [(32, 64), (64, 64), (128, 128), (96, 64), (32, 32), (16, 128), (128, 64)])
+def test_tile_classes_exact(kvs, BM, BN):
+    rng = np.random.default_rng(BM * 7 + BN)
+    announce(f"classify BM={BM} BN={BN}")
+    dev = torch.device("cuda:0")
+    for L in (1, 31, 64, 65, 200, 777):
+        for e in (inputs.evict_at_random(L, rng), inputs.evict_at_layout(L, 5, 40, 9, "last2"),
+                  np.full(L, np.iinfo(np.int32).max, dtype=np.int32)):
+            ev = torch.from_numpy(np.ascontiguousarray(e, dtype=np.int32)).to(dev)
+            got = kvs.kvs_classify_tiles(ev.view(1, L), BM, BN).cpu().numpy()
+            want = otiles.tile_classes(np.asarray(e), L, BM, BN).ravel()
+            np.testing.assert_array_equal(got, want)
+    # varlen packing, including an empty trace
+    lens = [65, 0, 200, 1, 130]
+    e = np.concatenate([inputs.evict_at_random(L, rng) for L in lens if L])
+    cu = torch.tensor(np.concatenate([[0], np.cumsum(lens)]), dtype=torch.int32, device=dev)
+    got = kvs.kvs_classify_tiles(torch.from_numpy(e).to(dev), BM, BN, cu_seqlens=cu).cpu().numpy()
+    np.testing.assert_array_equal(got, otiles.tile_classes_packed(e, lens, BM, BN))
+
+
+def test_tile_classes_of_workloads(kvs):
+    dev = torch.device("cuda:0")
+    for name in ("trace16k_gqa4", "trace64k_last2"):
+        wl = inputs.WORKLOADS[name]
+        e = wl.evict_at()
+        L = wl.lengths[0]
+        announce(f"classify {name}")
+        got = kvs.kvs_classify_tiles(torch.from_numpy(e).to(dev).view(1, L), 128, 128).cpu().numpy()
+        want = otiles.tile_classes(e, L, 128, 128).ravel()
+        np.testing.assert_array_equal(got, want)
+
+
+def test_check_evict_at(kvs):
+    dev = torch.device("cuda:0")
+    announce("check_evict_at")
+    e = inputs.evict_at_layout(500, 10, 50, 5, "keep_all")
+    ev = torch.from_numpy(e).to(dev)
+    assert kvs.kvs_check_evict_at(ev.view(1, 500)) == -1
+    bad = e.copy()
+    bad[321] = 321
+    bad[400] = 3
+    assert kvs.kvs_check_evict_at(torch.from_numpy(bad).to(dev).view(1, 500)) == 321
+    lens = [100, 400]
+    cu = torch.tensor([0, 100, 500], dtype=torch.int32, device=dev)
+    e2 = np.concatenate([inputs.evict_at_layout(100, 1, 9, 1), inputs.evict_at_layout(400, 3, 20, 2)])
+    assert kvs.kvs_check_evict_at(torch.from_numpy(e2).to(dev), cu) == -1
+    e2[150] = 50  # trace-local index 50 of trace 1: evict_at 50 <= 50
+    assert kvs.kvs_check_evict_at(torch.from_numpy(e2).to(dev), cu) == 150
+    badcu = torch.tensor([0, 300, 200], dtype=torch.int32, device=dev)
+    with pytest.raises(kvs.KvsError):
+        kvs.kvs_check_evict_at(torch.from_numpy(e2).to(dev), badcu)
