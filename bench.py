@@ -1,0 +1,193 @@
+"""Benchmark: eviction-masked attention forward + backward on one MI355X.
+
+One step = the library's forward call plus its backward call over one
+synthetic agent trace already resident in HBM (default: the 16,384-token
+keep-all-summaries trace, Hq=32, Hkv=8, D=128).  Throughput counts visible
+FLOPs only: 4*D per visible (query, key, q-head) triple in the forward and
+10*D in the backward.
+
+Prints one JSON line.  Also reports, for the kernel that takes the most time,
+its algorithmic FLOPs per launch over its average launch duration measured
+with HIP events on the launch stream ("roofline"), and the fp64 CPU checker
+timed on a bounded sample of the same workload ("cpu_baseline").
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu]
+"""
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "eviction-masked attn fwd+bwd TFLOP/s (visible FLOPs) and % bf16 MFMA peak"
+PEAK_BF16_TFLOPS = 2516.6          # MI355X dense bf16 MFMA, 256 CU x 2.4 GHz x 4096 FLOP/clk
+# Algorithmic FLOPs per visible (query, key, q-head) triple, in units of D.
+FLOPS_PER_VISIBLE = {"fwd": 4, "bwd_dkdv": 8, "bwd_dq": 2}   # dK/dV kernel: S, dP, dV, dK; dQ kernel: dQ
+KERNELS = ("classify", "fwd", "bwd_pre", "bwd_dkdv", "bwd_dq")
+
+
+def visible_pairs(evict_at, lengths):
+    tot, off = 0, 0
+    for L in lengths:
+        e = np.minimum(evict_at[off:off + L].astype(np.int64), L)
+        tot += int((e - np.arange(L)).sum())
+        off += L
+    return tot
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for f in ("kvs_kernels.hip", "kvs_device.h"):
+        with open(os.path.join(ROOT, "paper_2609_35750_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(kernel, workload):
+    """HBM bytes per launch from the committed counter summary, if it was taken
+    on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        rec = json.load(fh)
+    if rec.get("source_hash") != kernel_source_hash():
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(wl, tensors, evict_at, heads=2):
+    """The fp64 checker as it stands, timed on q-heads [0, heads) of KV head 0."""
+    from oracle import attention as orc
+
+    G = wl.G
+    heads = min(heads, G)
+    q = tensors["q"][:, :heads]
+    k, v = tensors["k"][:, :1], tensors["v"][:, :1]
+    do = tensors["do"][:, :heads]
+    cu = wl.cu_seqlens() if wl.varlen else None
+    t0 = time.perf_counter()
+    orc.backward(q, k, v, evict_at, wl.softmax_scale, do, cu_seqlens=cu)
+    dt = time.perf_counter() - t0
+    flops = 14 * wl.D * heads * visible_pairs(evict_at, wl.lengths)
+    try:
+        from threadpoolctl import threadpool_info
+
+        cores = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
+    except Exception:  # pragma: no cover
+        cores = len(os.sched_getaffinity(0))
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"fp64 forward+backward of q-heads 0..{heads - 1} with KV head 0 over the whole "
+                      f"{wl.name} workload ({flops / 1e12:.3f} visible TFLOP in {dt:.1f} s)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="trace16k_gqa4")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU checker timing")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (see DESIGN.md for how it would "
+              "shard); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2609_35750_amd import inputs, kvs
+
+    wl = inputs.WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    tensors = inputs.make_tensors(wl)
+    e = wl.evict_at()
+    vis = visible_pairs(e, wl.lengths)
+    f_fwd = 4 * wl.D * wl.Hq * vis
+    f_bwd = 10 * wl.D * wl.Hq * vis
+
+    if wl.varlen:
+        q, k, v, do = (tensors[x].to(dev) for x in ("q", "k", "v", "do"))
+        ev = torch.from_numpy(e).to(dev)
+        cu = torch.from_numpy(wl.cu_seqlens()).to(dev)
+        kw = dict(cu_seqlens=cu, max_seqlen=wl.T, check_cu=False)
+        kvs.kvs_evict_attn_fwd(q, k, v, ev, wl.softmax_scale, cu, wl.T)  # validates cu_seqlens once
+    else:
+        shp = lambda x: x.to(dev).view(1, wl.T, x.shape[1], wl.D)
+        q, k, v, do = (shp(tensors[x]) for x in ("q", "k", "v", "do"))
+        ev = torch.from_numpy(e).to(dev).view(1, wl.T)
+        kw = {}
+
+    o = torch.empty_like(q)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    lse = None
+
+    def step():
+        nonlocal lse
+        _, lse = kvs.kvs_evict_attn_fwd(q, k, v, ev, wl.softmax_scale, out=o, lse=lse, **kw)
+        kvs.kvs_evict_attn_bwd(do, q, k, v, o, lse, ev, wl.softmax_scale, dq=dq, dk=dk, dv=dv, **kw)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    kvs.kvs_prof_reset()
+    kvs.kvs_prof_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    kvs.kvs_prof_enable(False)
+    per_kernel = {}
+    for name in KERNELS:
+        n, ms = kvs.kvs_prof_read(name)
+        if n:
+            per_kernel[name] = {"launches": n, "avg_ms": ms / n}
+    kvs.kvs_prof_reset()
+
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    value = (f_fwd + f_bwd) / (ms_per_step * 1e-3) / 1e12
+
+    dom = max((k_ for k_ in per_kernel if k_ in FLOPS_PER_VISIBLE), key=lambda k_: per_kernel[k_]["avg_ms"])
+    flops_launch = FLOPS_PER_VISIBLE[dom] * wl.D * wl.Hq * vis
+    achieved = flops_launch / (per_kernel[dom]["avg_ms"] * 1e-3) / 1e12
+    roofline = {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": achieved / PEAK_BF16_TFLOPS, "traffic": load_traffic(dom, wl.name),
+                "kernel": dom, "avg_ms": per_kernel[dom]["avg_ms"],
+                "algorithmic_flops_per_launch": flops_launch}
+
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "traces": wl.B, "tokens": wl.ntok, "Hq": wl.Hq, "Hkv": wl.Hkv, "D": wl.D,
+                   "layout": {"prompt": wl.p, "turns": wl.w, "summary": wl.s, "strategy": wl.strategy},
+                   "visible_pairs_per_head": vis, "visible_tflop_per_step": (f_fwd + f_bwd) / 1e12},
+        "pct_of_bf16_peak": 100.0 * value / PEAK_BF16_TFLOPS,
+        "kernels_ms": {k_: round(v_["avg_ms"], 4) for k_, v_ in per_kernel.items()},
+        "roofline": roofline,
+    }
+    if not args.no_cpu:
+        out["cpu_baseline"] = cpu_baseline(wl, tensors, e)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
