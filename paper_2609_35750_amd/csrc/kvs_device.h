@@ -14,12 +14,12 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 typedef __attribute__((address_space(3))) uint16_t lds_u16;
+typedef __attribute__((address_space(3))) void lds_void;
 
 constexpr int kWave = 64;
 constexpr int kKeyTile = 64;      // keys per K/V tile of the row kernels (forward, dQ)
 constexpr int kColKeys = 128;     // keys per workgroup of the column kernel (dK, dV)
-constexpr int kQBlock = 32;       // query rows per step of the column kernel
-constexpr int kLdsPad = 8;        // bf16 elements of padding per LDS row
+constexpr int kQStep = 64;        // query rows staged per step of the column kernel
 
 enum TileClass : int { kEmpty = 0, kPartial = 1, kFull = 2 };
 
@@ -98,5 +98,49 @@ __device__ __forceinline__ uint2 pack4_bf16(float a, float b, float c, float d) 
 }
 
 __device__ __forceinline__ float wave_xor32(float x) { return __shfl_xor(x, 32); }
+
+// LDS tile of rows x D bf16 without padding.  Each row is D/8 chunks of 16
+// bytes; chunk c of row r is stored at chunk position c ^ swz(r).  The
+// permutation makes both access patterns of the MFMA operands free of bank
+// conflicts: 16 lanes reading the same chunk of 16 consecutive rows (b128
+// row reads), and 16-lane groups of the transposed read (4 rows x 32 bytes,
+// two groups side by side).
+template <int D>
+struct Swz {
+  static constexpr int CPR = D / 8;             // chunks per row
+  static constexpr int RPL = kWave / CPR;       // rows covered by one 64-lane 16-byte-per-lane load
+  __device__ static __forceinline__ int swz(int r) {
+    return D == 128 ? (((r & 3) << 2) | ((r >> 2) & 3)) : ((((r >> 1) & 1) << 2) | ((r >> 2) & 3));
+  }
+  // element offset of (row r, column col) inside the tile
+  __device__ static __forceinline__ int off(int r, int col) { return r * D + ((((col >> 3) ^ swz(r))) << 3) + (col & 7); }
+};
+
+// Issue asynchronous global -> LDS copies of tile rows [0, R) (global_load_lds_dwordx4:
+// lane l of a wave writes 16 bytes at the wave's LDS base + 16 l).  Row r of the
+// tile comes from global row min(row0 + r, rmax) (rows past the end of a trace
+// repeat its last row; callers mask them).  Waves split the rows.
+template <int D, int R>
+__device__ __forceinline__ void stage_rows(uint16_t* lds, const uint16_t* __restrict__ g, long long row_stride,
+                                           int row0, int rmax, int wave, int nwaves, int lane) {
+  constexpr int RPL = Swz<D>::RPL;
+  const int rl = lane / Swz<D>::CPR, p = lane % Swz<D>::CPR;
+  for (int rb = wave * RPL; rb < R; rb += nwaves * RPL) {
+    const int r = rb + rl;
+    const int c = p ^ Swz<D>::swz(r);
+    const int gr = min(row0 + r, rmax);
+    const uint16_t* src = g + gr * row_stride + c * 8;
+    __builtin_amdgcn_global_load_lds(src, (lds_void*)(lds + rb * D), 16, 0, 0);
+  }
+}
+
+// 64 consecutive 4-byte values (clamped at index imax) into LDS, by one wave.
+__device__ __forceinline__ void stage_words(void* lds, const void* __restrict__ g, int i0, int imax, int lane) {
+  const int i = min(i0 + lane, imax);
+  __builtin_amdgcn_global_load_lds((const char*)g + 4ll * i, (lds_void*)lds, 4, 0, 0);
+}
+
+// Wait for this wave's outstanding global loads (including LDS-direct ones).
+__device__ __forceinline__ void wait_vm() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 }  // namespace kvs

@@ -171,64 +171,14 @@ __device__ __forceinline__ int walker_next(TileWalker& w, const int2* __restrict
   return w.base + bit;
 }
 
-// ---------------------------------------------------------------- K/V tile staging (row kernels)
-template <int D>
-struct KVStage {
-  static constexpr int PITCH = D + kLdsPad;
-  static constexpr int CPR = D / 8;                       // 16-byte chunks per row
-  static constexpr int CHUNKS = kKeyTile * CPR;
-  static constexpr int MAXC = (CHUNKS + 255) / 256;       // per thread, >= 4 waves per workgroup
-  uint4 rk[MAXC], rv[MAXC];
-  int re;
-
-  __device__ __forceinline__ void load(const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
-                                       const int* __restrict__ evict, const Trace& tr, int Hkv, int g, int kt,
-                                       int tid, int nthr, bool with_v) {
-    const int j0 = kt * kKeyTile;
-#pragma unroll
-    for (int u = 0; u < MAXC; ++u) {
-      const int c = tid + u * nthr;
-      if (c < CHUNKS) {
-        const int r = c / CPR, cc = c % CPR;
-        const int j = j0 + r;
-        if (j < tr.L) {
-          const size_t off = ((size_t)(tr.tok0 + j) * Hkv + g) * D + cc * 8;
-          rk[u] = *reinterpret_cast<const uint4*>(K + off);
-          if (with_v) rv[u] = *reinterpret_cast<const uint4*>(V + off);
-        } else {
-          rk[u] = make_uint4(0, 0, 0, 0);
-          rv[u] = make_uint4(0, 0, 0, 0);
-        }
-      }
-    }
-    if (tid < kKeyTile) {
-      const int j = j0 + tid;
-      re = (j < tr.L) ? min(evict[tr.tok0 + j], tr.L) : 0;  // keys past the trace end are never visible
-    }
-  }
-
-  __device__ __forceinline__ void store(uint16_t* sK, uint16_t* sV, int* sE, int tid, int nthr, bool with_v) {
-#pragma unroll
-    for (int u = 0; u < MAXC; ++u) {
-      const int c = tid + u * nthr;
-      if (c < CHUNKS) {
-        const int r = c / CPR, cc = c % CPR;
-        *reinterpret_cast<uint4*>(sK + r * PITCH + cc * 8) = rk[u];
-        if (with_v) *reinterpret_cast<uint4*>(sV + r * PITCH + cc * 8) = rv[u];
-      }
-    }
-    if (tid < kKeyTile) sE[tid] = re;
-  }
-};
-
+// ---------------------------------------------------------------- operand reads from swizzled tiles
 // S^T block (32 keys x 32 queries) of the current tile: A = K rows from LDS, B = Q^T in registers.
 template <int D>
-__device__ __forceinline__ f32x16 scores_t(const uint16_t* sK, int kb, const bf16x8* qreg, int col, int half) {
-  constexpr int PITCH = D + kLdsPad;
+__device__ __forceinline__ f32x16 scores_t(const uint16_t* tile, int row0, const bf16x8* breg, int col, int half) {
   f32x16 s = {};
-  const uint16_t* base = sK + (32 * kb + col) * PITCH + 8 * half;
+  const int r = row0 + col;
 #pragma unroll
-  for (int ks = 0; ks < D / 16; ++ks) s = mfma32(lds_read_b128(base + 16 * ks), qreg[ks], s);
+  for (int ks = 0; ks < D / 16; ++ks) s = mfma32(lds_read_b128(tile + Swz<D>::off(r, 16 * ks + 8 * half)), breg[ks], s);
   return s;
 }
 
@@ -249,17 +199,17 @@ __device__ __forceinline__ void mask_t(f32x16& s, const int* sE, int kb, int j0,
   }
 }
 
-// A operand of a 32x32x16 MFMA read transposed from a row-major LDS tile:
-// rows (contraction index) r0 + {0..3} and r0 + 8 + {0..3} with r0 = 16 t + 4 half
+// A operand of a 32x32x16 MFMA read transposed from a swizzled tile: rows
+// (contraction index) r0 + {0..3} and r0 + 8 + {0..3} with r0 = row0 + 4 half
 // (the order in which the C layout of a score block lists its 16 values),
 // columns c0 + (l % 32).
-template <int PITCH>
+template <int D>
 __device__ __forceinline__ bf16x8 tr_operand(const uint16_t* tile, int row0, int c0, int lane) {
   const int li = lane & 15, g16 = lane >> 4;
   const int r = row0 + 4 * (g16 >> 1) + (li >> 2);
   const int c = c0 + 16 * (g16 & 1) + 4 * (li & 3);
-  const s16x4 lo = lds_read_tr(tile + r * PITCH + c);
-  const s16x4 hi = lds_read_tr(tile + (r + 8) * PITCH + c);
+  const s16x4 lo = lds_read_tr(tile + Swz<D>::off(r, c));
+  const s16x4 hi = lds_read_tr(tile + Swz<D>::off(r + 8, c));
   return cat_tr(lo, hi);
 }
 
@@ -290,19 +240,36 @@ __device__ __forceinline__ bool row_tile(const RowArgs& a, RowTile& t) {
   return true;
 }
 
+// Asynchronous staging of one 64-key K/V (and evict_at) tile of KV head g.
+template <int D>
+__device__ __forceinline__ void stage_kv(uint16_t* sK, uint16_t* sV, int* sE, const RowArgs& a, const RowTile& rt,
+                                         int kt, int wave, int nw, int lane) {
+  const int j0 = kt * kKeyTile;
+  const long long base = ((long long)rt.tr.tok0 * a.Hkv + rt.g) * D;
+  const long long stride = (long long)a.Hkv * D;
+  stage_rows<D, kKeyTile>(sK, a.k + base, stride, j0, rt.tr.L - 1, wave, nw, lane);
+  stage_rows<D, kKeyTile>(sV, a.v + base, stride, j0, rt.tr.L - 1, wave, nw, lane);
+  if (wave == nw - 1) stage_words(sE, a.evict + rt.tr.tok0, j0, rt.tr.L - 1, lane);
+}
+
 // ---------------------------------------------------------------- forward
+// The K/V tiles are double-buffered in two distinct LDS arrays each; the loop
+// body alternates between them so the compiler can tell that the
+// asynchronous fill of the next buffer never aliases the reads of the
+// current one (and does not wait for the fill before reading).
 template <int D>
 __global__ void __launch_bounds__(512) fwd_kernel(RowArgs a) {
   constexpr int KS = D / 16, DB = D / 32;
-  using Stage = KVStage<D>;
-  constexpr int PITCH = Stage::PITCH;
-  __shared__ __attribute__((aligned(16))) uint16_t sK[2][kKeyTile * PITCH];
-  __shared__ __attribute__((aligned(16))) uint16_t sV[2][kKeyTile * PITCH];
-  __shared__ __attribute__((aligned(16))) int sE[2][kKeyTile];
+  __shared__ __attribute__((aligned(1024))) uint16_t sK0[kKeyTile * D];
+  __shared__ __attribute__((aligned(1024))) uint16_t sK1[kKeyTile * D];
+  __shared__ __attribute__((aligned(1024))) uint16_t sV0[kKeyTile * D];
+  __shared__ __attribute__((aligned(1024))) uint16_t sV1[kKeyTile * D];
+  __shared__ __attribute__((aligned(256))) int sE0[kKeyTile];
+  __shared__ __attribute__((aligned(256))) int sE1[kKeyTile];
 
   RowTile rt;
   if (!row_tile(a, rt)) return;
-  const int tid = threadIdx.x, nthr = blockDim.x, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = blockDim.x >> 6;
   const int half = lane >> 5, col = lane & 31;
   const Trace tr = rt.tr;
   const int i = rt.i0w + col;
@@ -310,10 +277,9 @@ __global__ void __launch_bounds__(512) fwd_kernel(RowArgs a) {
 
   bf16x8 qreg[KS];
   {
-    const uint16_t* qrow = a.q + ((size_t)(tr.tok0 + (row_ok ? i : 0)) * a.Hq + rt.h) * D + 8 * half;
+    const uint16_t* qrow = a.q + ((size_t)(tr.tok0 + min(i, tr.L - 1)) * a.Hq + rt.h) * D + 8 * half;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      qreg[ks] = row_ok ? as_bf16x8(*reinterpret_cast<const uint4*>(qrow + 16 * ks)) : bf16x8{};
+    for (int ks = 0; ks < KS; ++ks) qreg[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(qrow + 16 * ks));
   }
 
   f32x16 acc[DB];
@@ -324,37 +290,34 @@ __global__ void __launch_bounds__(512) fwd_kernel(RowArgs a) {
   const int kidx0 = kstat_index(rt.b, tr.tok0, 0, kKeyTile);
   TileWalker w{0, (min(rt.i1, tr.L) + kKeyTile - 1) / kKeyTile, 0ull, 0ull};
   walker_load(w, a.kstats, kidx0, rt.i0, rt.i1, tr.L);
-  int kt = walker_next(w, a.kstats, kidx0, rt.i0, rt.i1, tr.L);
+  int kt = __builtin_amdgcn_readfirstlane(walker_next(w, a.kstats, kidx0, rt.i0, rt.i1, tr.L));
+  int2 kst = kt >= 0 ? a.kstats[kidx0 + kt] : make_int2(0, 0);
 
-  Stage st;
-  if (kt >= 0) {
-    st.load(a.k, a.v, a.evict, tr, a.Hkv, rt.g, kt, tid, nthr, true);
-    st.store(sK[0], sV[0], sE[0], tid, nthr, true);
-  }
-  __syncthreads();
-  int buf = 0;
-  while (kt >= 0) {
-    const int nkt = walker_next(w, a.kstats, kidx0, rt.i0, rt.i1, tr.L);
-    if (nkt >= 0) st.load(a.k, a.v, a.evict, tr, a.Hkv, rt.g, nkt, tid, nthr, true);
-
+  // One tile: prefetch the next tile into (nK, nV, nE), compute on (cK, cV, cE).
+  auto body = [&](const uint16_t* cK, const uint16_t* cV, const int* cE, uint16_t* nK, uint16_t* nV, int* nE) {
+    // Statistics of the next tile are read before its copy is issued and used one
+    // iteration later, so no wait on this iteration's copies is needed for them.
+    const int nkt = __builtin_amdgcn_readfirstlane(walker_next(w, a.kstats, kidx0, rt.i0, rt.i1, tr.L));
+    int2 nkst = make_int2(0, 0);
+    if (nkt >= 0) {
+      nkst = a.kstats[kidx0 + nkt];
+      stage_kv<D>(nK, nV, nE, a, rt, nkt, wave, nw, lane);
+    }
     const int j0 = kt * kKeyTile;
-    const int2 ks_ = a.kstats[kidx0 + kt];
-    const int cls = tile_class(rt.i0w, rt.i0w + 32, j0, j0 + kKeyTile, tr.L, ks_.x, ks_.y);
+    const int cls = tile_class(rt.i0w, rt.i0w + 32, j0, j0 + kKeyTile, tr.L, kst.x, kst.y);
     if (cls != kEmpty) {
       f32x16 s[2];
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
-        s[kb] = scores_t<D>(sK[buf], kb, qreg, col, half);
-#pragma unroll
-        for (int r = 0; r < 16; ++r) s[kb][r] *= a.scale_log2;
-        if (cls == kPartial) mask_t(s[kb], sE[buf], kb, j0, i, tr.L, half);
+        s[kb] = scores_t<D>(cK, 32 * kb, qreg, col, half);
+        if (cls == kPartial) mask_t(s[kb], cE, kb, j0, i, tr.L, half);
       }
       float mx = -INFINITY;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
-      mx = fmaxf(mx, wave_xor32(mx));
+      mx = fmaxf(mx, wave_xor32(mx)) * a.scale_log2;
       const float m_new = fmaxf(m_run, mx);
       const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
@@ -363,16 +326,18 @@ __global__ void __launch_bounds__(512) fwd_kernel(RowArgs a) {
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float p = __builtin_amdgcn_exp2f(s[kb][r] - m_use);
+          const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][r], a.scale_log2, -m_use));
           s[kb][r] = p;
           ls += p;
         }
       l_run = l_run * alpha + ls;
       m_run = m_new;
+      if (alpha != 1.f) {
 #pragma unroll
-      for (int d = 0; d < DB; ++d)
+        for (int d = 0; d < DB; ++d)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) acc[d][r] *= alpha;
+          for (int r = 0; r < 16; ++r) acc[d][r] *= alpha;
+      }
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -380,13 +345,22 @@ __global__ void __launch_bounds__(512) fwd_kernel(RowArgs a) {
           const bf16x8 pb = pack8(s[kb], 8 * t);
 #pragma unroll
           for (int d = 0; d < DB; ++d)
-            acc[d] = mfma32(tr_operand<PITCH>(sV[buf], 32 * kb + 16 * t, 32 * d, lane), pb, acc[d]);
+            acc[d] = mfma32(tr_operand<D>(cV, 32 * kb + 16 * t, 32 * d, lane), pb, acc[d]);
         }
     }
-    if (nkt >= 0) st.store(sK[buf ^ 1], sV[buf ^ 1], sE[buf ^ 1], tid, nthr, true);
+    wait_vm();
     __syncthreads();
-    buf ^= 1;
     kt = nkt;
+    kst = nkst;
+  };
+
+  if (kt >= 0) stage_kv<D>(sK0, sV0, sE0, a, rt, kt, wave, nw, lane);
+  wait_vm();
+  __syncthreads();
+  while (kt >= 0) {
+    body(sK0, sV0, sE0, sK1, sV1, sE1);
+    if (kt < 0) break;
+    body(sK1, sV1, sE1, sK0, sV0, sE0);
   }
 
   const float l_tot = l_run + wave_xor32(l_run);
@@ -438,34 +412,34 @@ __global__ void __launch_bounds__(256) bwd_pre_kernel(const uint16_t* __restrict
 template <int D>
 __global__ void __launch_bounds__(512) dq_kernel(RowArgs a) {
   constexpr int KS = D / 16, DB = D / 32;
-  using Stage = KVStage<D>;
-  constexpr int PITCH = Stage::PITCH;
-  __shared__ __attribute__((aligned(16))) uint16_t sK[2][kKeyTile * PITCH];
-  __shared__ __attribute__((aligned(16))) uint16_t sV[2][kKeyTile * PITCH];
-  __shared__ __attribute__((aligned(16))) int sE[2][kKeyTile];
+  __shared__ __attribute__((aligned(1024))) uint16_t sK0[kKeyTile * D];
+  __shared__ __attribute__((aligned(1024))) uint16_t sK1[kKeyTile * D];
+  __shared__ __attribute__((aligned(1024))) uint16_t sV0[kKeyTile * D];
+  __shared__ __attribute__((aligned(1024))) uint16_t sV1[kKeyTile * D];
+  __shared__ __attribute__((aligned(256))) int sE0[kKeyTile];
+  __shared__ __attribute__((aligned(256))) int sE1[kKeyTile];
 
   RowTile rt;
   if (!row_tile(a, rt)) return;
-  const int tid = threadIdx.x, nthr = blockDim.x, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = blockDim.x >> 6;
   const int half = lane >> 5, col = lane & 31;
   const Trace tr = rt.tr;
   const int i = rt.i0w + col;
   const bool row_ok = i < tr.L;
+  const int ic = min(i, tr.L - 1);
 
   bf16x8 qreg[KS], oreg[KS];
-  float lse2 = 0.f, dlt = 0.f;
+  float lse2, dlt;
   {
-    const size_t roff = ((size_t)(tr.tok0 + (row_ok ? i : 0)) * a.Hq + rt.h) * D + 8 * half;
+    const size_t roff = ((size_t)(tr.tok0 + ic) * a.Hq + rt.h) * D + 8 * half;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      qreg[ks] = row_ok ? as_bf16x8(*reinterpret_cast<const uint4*>(a.q + roff + 16 * ks)) : bf16x8{};
-      oreg[ks] = row_ok ? as_bf16x8(*reinterpret_cast<const uint4*>(a.dout + roff + 16 * ks)) : bf16x8{};
+      qreg[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(a.q + roff + 16 * ks));
+      oreg[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(a.dout + roff + 16 * ks));
     }
-    if (row_ok) {
-      const long long li = lse_index(a.varlen, a.ntok, a.Hq, a.T, rt.b, rt.h, tr.tok0, i);
-      lse2 = a.lse_in[li] * 1.4426950408889634f;
-      dlt = a.delta[li];
-    }
+    const long long li = lse_index(a.varlen, a.ntok, a.Hq, a.T, rt.b, rt.h, tr.tok0, ic);
+    lse2 = a.lse_in[li] * 1.4426950408889634f;
+    dlt = a.delta[li];
   }
 
   f32x16 acc[DB];
@@ -475,33 +449,29 @@ __global__ void __launch_bounds__(512) dq_kernel(RowArgs a) {
   const int kidx0 = kstat_index(rt.b, tr.tok0, 0, kKeyTile);
   TileWalker w{0, (min(rt.i1, tr.L) + kKeyTile - 1) / kKeyTile, 0ull, 0ull};
   walker_load(w, a.kstats, kidx0, rt.i0, rt.i1, tr.L);
-  int kt = walker_next(w, a.kstats, kidx0, rt.i0, rt.i1, tr.L);
+  int kt = __builtin_amdgcn_readfirstlane(walker_next(w, a.kstats, kidx0, rt.i0, rt.i1, tr.L));
+  int2 kst = kt >= 0 ? a.kstats[kidx0 + kt] : make_int2(0, 0);
 
-  Stage st;
-  if (kt >= 0) {
-    st.load(a.k, a.v, a.evict, tr, a.Hkv, rt.g, kt, tid, nthr, true);
-    st.store(sK[0], sV[0], sE[0], tid, nthr, true);
-  }
-  __syncthreads();
-  int buf = 0;
-  while (kt >= 0) {
-    const int nkt = walker_next(w, a.kstats, kidx0, rt.i0, rt.i1, tr.L);
-    if (nkt >= 0) st.load(a.k, a.v, a.evict, tr, a.Hkv, rt.g, nkt, tid, nthr, true);
-
+  auto body = [&](const uint16_t* cK, const uint16_t* cV, const int* cE, uint16_t* nK, uint16_t* nV, int* nE) {
+    // Statistics of the next tile are read before its copy is issued and used one
+    // iteration later, so no wait on this iteration's copies is needed for them.
+    const int nkt = __builtin_amdgcn_readfirstlane(walker_next(w, a.kstats, kidx0, rt.i0, rt.i1, tr.L));
+    int2 nkst = make_int2(0, 0);
+    if (nkt >= 0) {
+      nkst = a.kstats[kidx0 + nkt];
+      stage_kv<D>(nK, nV, nE, a, rt, nkt, wave, nw, lane);
+    }
     const int j0 = kt * kKeyTile;
-    const int2 ks_ = a.kstats[kidx0 + kt];
-    const int cls = tile_class(rt.i0w, rt.i0w + 32, j0, j0 + kKeyTile, tr.L, ks_.x, ks_.y);
+    const int cls = tile_class(rt.i0w, rt.i0w + 32, j0, j0 + kKeyTile, tr.L, kst.x, kst.y);
     if (cls != kEmpty) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
-        f32x16 s = scores_t<D>(sK[buf], kb, qreg, col, half);
-#pragma unroll
-        for (int r = 0; r < 16; ++r) s[r] = s[r] * a.scale_log2 - lse2;
-        if (cls == kPartial) mask_t(s, sE[buf], kb, j0, i, tr.L, half);
-        f32x16 dp = scores_t<D>(sV[buf], kb, oreg, col, half);
+        f32x16 s = scores_t<D>(cK, 32 * kb, qreg, col, half);
+        if (cls == kPartial) mask_t(s, cE, kb, j0, i, tr.L, half);
+        const f32x16 dp = scores_t<D>(cV, 32 * kb, oreg, col, half);
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float p = __builtin_amdgcn_exp2f(s[r]);
+          const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], a.scale_log2, -lse2));
           s[r] = p * (dp[r] - dlt);
         }
 #pragma unroll
@@ -509,14 +479,23 @@ __global__ void __launch_bounds__(512) dq_kernel(RowArgs a) {
           const bf16x8 dsb = pack8(s, 8 * t);
 #pragma unroll
           for (int d = 0; d < DB; ++d)
-            acc[d] = mfma32(tr_operand<PITCH>(sK[buf], 32 * kb + 16 * t, 32 * d, lane), dsb, acc[d]);
+            acc[d] = mfma32(tr_operand<D>(cK, 32 * kb + 16 * t, 32 * d, lane), dsb, acc[d]);
         }
       }
     }
-    if (nkt >= 0) st.store(sK[buf ^ 1], sV[buf ^ 1], sE[buf ^ 1], tid, nthr, true);
+    wait_vm();
     __syncthreads();
-    buf ^= 1;
     kt = nkt;
+    kst = nkst;
+  };
+
+  if (kt >= 0) stage_kv<D>(sK0, sV0, sE0, a, rt, kt, wave, nw, lane);
+  wait_vm();
+  __syncthreads();
+  while (kt >= 0) {
+    body(sK0, sV0, sE0, sK1, sV1, sE1);
+    if (kt < 0) break;
+    body(sK1, sV1, sE1, sK0, sV0, sE0);
   }
 
   if (row_ok) {
@@ -536,14 +515,14 @@ __global__ void __launch_bounds__(512) dq_kernel(RowArgs a) {
 template <int D>
 __global__ void __launch_bounds__(256) dkdv_kernel(ColArgs a) {
   constexpr int KS = D / 16, DB = D / 32;
-  constexpr int PITCH = D + kLdsPad;
-  constexpr int CPR = D / 8;
-  constexpr int CHUNKS = kQBlock * CPR;       // per tensor
-  constexpr int MAXC = (CHUNKS + 255) / 256;
-  __shared__ __attribute__((aligned(16))) uint16_t sQ[2][kQBlock * PITCH];
-  __shared__ __attribute__((aligned(16))) uint16_t sO[2][kQBlock * PITCH];
-  __shared__ __attribute__((aligned(16))) float sL[2][kQBlock];
-  __shared__ __attribute__((aligned(16))) float sD[2][kQBlock];
+  __shared__ __attribute__((aligned(1024))) uint16_t sQ0[kQStep * D];
+  __shared__ __attribute__((aligned(1024))) uint16_t sQ1[kQStep * D];
+  __shared__ __attribute__((aligned(1024))) uint16_t sO0[kQStep * D];
+  __shared__ __attribute__((aligned(1024))) uint16_t sO1[kQStep * D];
+  __shared__ __attribute__((aligned(256))) float sL0[kQStep];
+  __shared__ __attribute__((aligned(256))) float sL1[kQStep];
+  __shared__ __attribute__((aligned(256))) float sD0[kQStep];
+  __shared__ __attribute__((aligned(256))) float sD1[kQStep];
   __shared__ int sEmax[4];
 
   int wg = blockIdx.x;
@@ -561,6 +540,7 @@ __global__ void __launch_bounds__(256) dkdv_kernel(ColArgs a) {
   const int jw0 = j0 + 32 * wave;
   const int j = jw0 + col;
   const bool key_ok = j < tr.L;
+  const int jc = min(j, tr.L - 1);
   const int ej = key_ok ? min(a.evict[tr.tok0 + j], tr.L) : 0;
   int emin_w = key_ok ? ej : INT_MAX, emax_w = key_ok ? ej : INT_MIN;
 #pragma unroll
@@ -572,18 +552,18 @@ __global__ void __launch_bounds__(256) dkdv_kernel(ColArgs a) {
 
   bf16x8 kreg[KS], vreg[KS];
   {
-    const size_t koff = ((size_t)(tr.tok0 + (key_ok ? j : 0)) * a.Hkv + g) * D + 8 * half;
+    const size_t koff = ((size_t)(tr.tok0 + jc) * a.Hkv + g) * D + 8 * half;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      kreg[ks] = key_ok ? as_bf16x8(*reinterpret_cast<const uint4*>(a.k + koff + 16 * ks)) : bf16x8{};
-      vreg[ks] = key_ok ? as_bf16x8(*reinterpret_cast<const uint4*>(a.v + koff + 16 * ks)) : bf16x8{};
+      kreg[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(a.k + koff + 16 * ks));
+      vreg[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(a.v + koff + 16 * ks));
     }
   }
   __syncthreads();
   const int emax_wg = max(max(sEmax[0], sEmax[1]), max(sEmax[2], sEmax[3]));
-  const int qb_lo = j0 / kQBlock;
-  const int qb_hi = (emax_wg + kQBlock - 1) / kQBlock;
-  const int steps = (qb_hi - qb_lo) * a.G;
+  const int qs_lo = j0 / kQStep;
+  const int qs_hi = (emax_wg + kQStep - 1) / kQStep;
+  const int steps = (qs_hi - qs_lo) * a.G;
 
   f32x16 dk[DB], dv[DB];
 #pragma unroll
@@ -592,96 +572,55 @@ __global__ void __launch_bounds__(256) dkdv_kernel(ColArgs a) {
     dv[d] = f32x16{};
   }
 
-  uint4 rq[MAXC], ro[MAXC];
-  float rl = 0.f;
-  auto load = [&](int step) {
-    const int qb = qb_lo + step / a.G;
+  auto stage = [&](uint16_t* q_, uint16_t* o_, float* l_, float* d_, int step) {
+    const int i0 = (qs_lo + step / a.G) * kQStep;
     const int h = g * a.G + step % a.G;
-    const int i0 = qb * kQBlock;
-#pragma unroll
-    for (int u = 0; u < MAXC; ++u) {
-      const int c = tid + u * 256;
-      if (c < CHUNKS) {
-        const int r = c / CPR, cc = c % CPR;
-        const int i = i0 + r;
-        if (i < tr.L) {
-          const size_t off = ((size_t)(tr.tok0 + i) * a.Hq + h) * D + cc * 8;
-          rq[u] = *reinterpret_cast<const uint4*>(a.q + off);
-          ro[u] = *reinterpret_cast<const uint4*>(a.dout + off);
-        } else {
-          rq[u] = make_uint4(0, 0, 0, 0);
-          ro[u] = make_uint4(0, 0, 0, 0);
-        }
-      }
-    }
-    if (tid < 2 * kQBlock) {
-      const int i = i0 + (tid & 31);
-      if (i < tr.L) {
-        const long long li = lse_index(a.varlen, a.ntok, a.Hq, a.T, b, h, tr.tok0, i);
-        rl = (tid < kQBlock) ? a.lse[li] * 1.4426950408889634f : a.delta[li];
-      } else {
-        rl = 0.f;
-      }
-    }
-  };
-  auto store = [&](int bufi) {
-#pragma unroll
-    for (int u = 0; u < MAXC; ++u) {
-      const int c = tid + u * 256;
-      if (c < CHUNKS) {
-        const int r = c / CPR, cc = c % CPR;
-        *reinterpret_cast<uint4*>(&sQ[bufi][r * PITCH + cc * 8]) = rq[u];
-        *reinterpret_cast<uint4*>(&sO[bufi][r * PITCH + cc * 8]) = ro[u];
-      }
-    }
-    if (tid < kQBlock) sL[bufi][tid] = rl;
-    else if (tid < 2 * kQBlock) sD[bufi][tid - kQBlock] = rl;
+    const long long base = ((long long)tr.tok0 * a.Hq + h) * D;
+    stage_rows<D, kQStep>(q_, a.q + base, (long long)a.Hq * D, i0, tr.L - 1, wave, 4, lane);
+    stage_rows<D, kQStep>(o_, a.dout + base, (long long)a.Hq * D, i0, tr.L - 1, wave, 4, lane);
+    const long long lb = lse_index(a.varlen, a.ntok, a.Hq, a.T, b, h, tr.tok0, 0);
+    if (wave == 0) stage_words(l_, a.lse + lb, i0, tr.L - 1, lane);
+    if (wave == 1) stage_words(d_, a.delta + lb, i0, tr.L - 1, lane);
   };
 
-  if (steps > 0) {
-    load(0);
-    store(0);
-  }
-  __syncthreads();
-  int buf = 0;
-  for (int step = 0; step < steps; ++step) {
-    const bool more = step + 1 < steps;
-    if (more) load(step + 1);
-    const int qb = qb_lo + step / a.G;
-    const int i0 = qb * kQBlock;
-    const int cls = tile_class(i0, i0 + kQBlock, jw0, jw0 + 32, tr.L, emin_w, emax_w);
-    if (cls != kEmpty) {
-      // S = Q K^T (rows i, columns = this wave's 32 keys)
-      f32x16 s = {};
-      f32x16 dp = {};
-      {
-        const uint16_t* qb_ = &sQ[buf][col * PITCH + 8 * half];
-        const uint16_t* ob_ = &sO[buf][col * PITCH + 8 * half];
+  int step = 0;
+  // One step: prefetch step + 1 into the other buffers, compute on (cQ, cO, cL, cD).
+  auto body = [&](const uint16_t* cQ, const uint16_t* cO, const float* cL, const float* cD, uint16_t* nQ,
+                  uint16_t* nO, float* nL, float* nD) {
+    if (step + 1 < steps) stage(nQ, nO, nL, nD, step + 1);
+    const int i0 = (qs_lo + step / a.G) * kQStep;
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          s = mfma32(lds_read_b128(qb_ + 16 * ks), kreg[ks], s);
-          dp = mfma32(lds_read_b128(ob_ + 16 * ks), vreg[ks], dp);
-        }
-      }
-      float lrow[16], drow[16];
+    for (int sb = 0; sb < kQStep / 32; ++sb) {
+      const int ib = i0 + 32 * sb;
+      const int cls = tile_class(ib, ib + 32, jw0, jw0 + 32, tr.L, emin_w, emax_w);
+      if (cls == kEmpty) continue;
+      // S = Q K^T and dP = dO V^T for 32 rows x this wave's 32 keys (C layout: lane <-> key).
+      f32x16 s = {}, dp = {};
 #pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        const float4 l4 = *reinterpret_cast<const float4*>(&sL[buf][8 * q4 + 4 * half]);
-        const float4 d4 = *reinterpret_cast<const float4*>(&sD[buf][8 * q4 + 4 * half]);
-        lrow[4 * q4] = l4.x; lrow[4 * q4 + 1] = l4.y; lrow[4 * q4 + 2] = l4.z; lrow[4 * q4 + 3] = l4.w;
-        drow[4 * q4] = d4.x; drow[4 * q4 + 1] = d4.y; drow[4 * q4 + 2] = d4.z; drow[4 * q4 + 3] = d4.w;
+      for (int ks = 0; ks < KS; ++ks) {
+        const int o = Swz<D>::off(32 * sb + col, 16 * ks + 8 * half);
+        s = mfma32(lds_read_b128(cQ + o), kreg[ks], s);
+        dp = mfma32(lds_read_b128(cO + o), vreg[ks], dp);
       }
       f32x16 p, ds;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float x = s[r] * a.scale_log2 - lrow[r];
-        if (cls == kPartial) {
-          const int i = i0 + 8 * (r >> 2) + 4 * half + (r & 3);
-          const bool vis = (j <= i) && (i < ej) && (i < tr.L);
-          if (!vis) x = -INFINITY;
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int rr = 32 * sb + 8 * q4 + 4 * half;
+        const float4 l4 = *reinterpret_cast<const float4*>(cL + rr);
+        const float4 d4 = *reinterpret_cast<const float4*>(cD + rr);
+        const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
+        const float dv4[4] = {d4.x, d4.y, d4.z, d4.w};
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const int r = 4 * q4 + t;
+          float x = __builtin_fmaf(s[r], a.scale_log2, -lv[t] * 1.4426950408889634f);
+          if (cls == kPartial) {
+            const int ii = ib + 8 * q4 + 4 * half + t;
+            if (!((j <= ii) && (ii < ej) && (ii < tr.L))) x = -INFINITY;
+          }
+          p[r] = __builtin_amdgcn_exp2f(x);
+          ds[r] = p[r] * (dp[r] - dv4[t]);
         }
-        p[r] = __builtin_amdgcn_exp2f(x);
-        ds[r] = p[r] * (dp[r] - drow[r]);
       }
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
@@ -689,14 +628,23 @@ __global__ void __launch_bounds__(256) dkdv_kernel(ColArgs a) {
         const bf16x8 dsb = pack8(ds, 8 * t);
 #pragma unroll
         for (int d = 0; d < DB; ++d) {
-          dv[d] = mfma32(tr_operand<PITCH>(sO[buf], 16 * t, 32 * d, lane), pb, dv[d]);
-          dk[d] = mfma32(tr_operand<PITCH>(sQ[buf], 16 * t, 32 * d, lane), dsb, dk[d]);
+          dv[d] = mfma32(tr_operand<D>(cO, 32 * sb + 16 * t, 32 * d, lane), pb, dv[d]);
+          dk[d] = mfma32(tr_operand<D>(cQ, 32 * sb + 16 * t, 32 * d, lane), dsb, dk[d]);
         }
       }
     }
-    if (more) store(buf ^ 1);
+    wait_vm();
     __syncthreads();
-    buf ^= 1;
+    ++step;
+  };
+
+  if (steps > 0) stage(sQ0, sO0, sL0, sD0, 0);
+  wait_vm();
+  __syncthreads();
+  while (step < steps) {
+    body(sQ0, sO0, sL0, sD0, sQ1, sO1, sL1, sD1);
+    if (step >= steps) break;
+    body(sQ1, sO1, sL1, sD1, sQ0, sO0, sL0, sD0);
   }
 
   if (key_ok) {
