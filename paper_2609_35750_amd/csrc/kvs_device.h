@@ -99,40 +99,77 @@ __device__ __forceinline__ uint2 pack4_bf16(float a, float b, float c, float d) 
 
 __device__ __forceinline__ float wave_xor32(float x) { return __shfl_xor(x, 32); }
 
-// LDS tile of rows x D bf16 without padding.  Each row is D/8 chunks of 16
-// bytes; chunk c of row r is stored at chunk position c ^ swz(r).  The
-// permutation makes both access patterns of the MFMA operands free of bank
-// conflicts: 16 lanes reading the same chunk of 16 consecutive rows (b128
-// row reads), and 16-lane groups of the transposed read (4 rows x 32 bytes,
-// two groups side by side).
+// LDS tile of rows x D bf16.  Rows are padded (D = 128: 144 elements, D = 64:
+// 72) and, for D = 128, the lowest bit of the 16-byte chunk index is flipped
+// in rows 8..15 of every 16.  Two access patterns are then free of bank
+// conflicts: 16 lanes reading the same chunk of 16 consecutive rows (b128 reads
+// of MFMA operands), and the 4-row x 32-byte block of each 16-lane group of a
+// transposed read.  Because the flip only touches bit 0 of the chunk index and
+// depends only on the row modulo 16, moving by whole k-steps (32 bytes), by
+// 32-column blocks or by 16-row blocks is a constant offset, so every operand
+// read is a per-lane base plus an immediate.
 template <int D>
-struct Swz {
-  static constexpr int CPR = D / 8;             // chunks per row
-  static constexpr int RPL = kWave / CPR;       // rows covered by one 64-lane 16-byte-per-lane load
-  __device__ static __forceinline__ int swz(int r) {
-    return D == 128 ? (((r & 3) << 2) | ((r >> 2) & 3)) : ((((r >> 1) & 1) << 2) | ((r >> 2) & 3));
+struct Lay {
+  static constexpr int PITCH = D == 128 ? 144 : 72;   // bf16 elements per LDS row
+  static constexpr int CPR = D / 8;                    // 16-byte data chunks per row
+  static constexpr int CPRP = PITCH / 8;               // chunks per padded row
+  __device__ static __forceinline__ int flip(int r) { return D == 128 ? ((r >> 3) & 1) : 0; }
+  __device__ static __forceinline__ int off(int r, int col) { return r * PITCH + (((col >> 3) ^ flip(r)) << 3) + (col & 7); }
+  // b128 operand read of row (row0 + l % 32), columns 8 (l / 32) .. +7 of k-step 0;
+  // add row0 * PITCH + 16 ks (row0 a multiple of 16).
+  __device__ static __forceinline__ int row_lane(int lane) { return off(lane & 31, 8 * (lane >> 5)); }
+  // transposed operand reads (see tr_operand): rows 4 (g16 / 2) + (li / 4) and +8,
+  // columns 16 (g16 % 2) + 4 (li % 4); add row0 * PITCH + c0 (row0 % 16 == 0, c0 % 32 == 0).
+  __device__ static __forceinline__ int tr_lo(int lane) {
+    const int li = lane & 15, g16 = lane >> 4;
+    return off(4 * (g16 >> 1) + (li >> 2), 16 * (g16 & 1) + 4 * (li & 3));
   }
-  // element offset of (row r, column col) inside the tile
-  __device__ static __forceinline__ int off(int r, int col) { return r * D + ((((col >> 3) ^ swz(r))) << 3) + (col & 7); }
+  __device__ static __forceinline__ int tr_hi(int lane) {
+    const int li = lane & 15, g16 = lane >> 4;
+    return off(8 + 4 * (g16 >> 1) + (li >> 2), 16 * (g16 & 1) + 4 * (li & 3));
+  }
 };
 
-// Issue asynchronous global -> LDS copies of tile rows [0, R) (global_load_lds_dwordx4:
-// lane l of a wave writes 16 bytes at the wave's LDS base + 16 l).  Row r of the
-// tile comes from global row min(row0 + r, rmax) (rows past the end of a trace
-// repeat its last row; callers mask them).  Waves split the rows.
-template <int D, int R>
-__device__ __forceinline__ void stage_rows(uint16_t* lds, const uint16_t* __restrict__ g, long long row_stride,
-                                           int row0, int rmax, int wave, int nwaves, int lane) {
-  constexpr int RPL = Swz<D>::RPL;
-  const int rl = lane / Swz<D>::CPR, p = lane % Swz<D>::CPR;
-  for (int rb = wave * RPL; rb < R; rb += nwaves * RPL) {
-    const int r = rb + rl;
-    const int c = p ^ Swz<D>::swz(r);
-    const int gr = min(row0 + r, rmax);
-    const uint16_t* src = g + gr * row_stride + c * 8;
-    __builtin_amdgcn_global_load_lds(src, (lds_void*)(lds + rb * D), 16, 0, 0);
+// Asynchronous global -> LDS copies of an R-row tile (global_load_lds_dwordx4:
+// lane l of a wave writes 16 bytes at the wave's LDS base + 16 l, so the 64
+// lanes of one instruction fill 64 consecutive 16-byte slots of the padded
+// tile; padding slots are skipped).  Waves take turns issuing the 64-slot
+// pieces: wave w issues pieces w, w + nw, ...  The per-lane tile row and column
+// of every piece are computed once (init) so that issuing a tile costs a
+// clamp and an address per piece.  Row r of the tile comes from global row
+// min(row0 + r, rmax) (rows past the end of a trace repeat its last row;
+// callers mask them).
+template <int D, int R, int MAXI>
+struct RowStager {
+  using LY = Lay<D>;
+  static constexpr int NI = R * LY::CPRP / kWave;   // 64-slot pieces per tile
+  static_assert(R * LY::CPRP % kWave == 0, "tile must fill whole 64-slot pieces");
+  int row[MAXI];   // tile row of this lane's slot, or -1 (padding or no piece)
+  int col[MAXI];   // element column of the slot's first element in the source row
+
+  __device__ __forceinline__ void init(int wave, int nw, int lane) {
+#pragma unroll
+    for (int i = 0; i < MAXI; ++i) {
+      const int n = wave + i * nw;
+      const int q = n * kWave + lane;
+      const int r = q / LY::CPRP, pc = q - r * LY::CPRP;
+      const bool ok = n < NI && pc < LY::CPR;
+      row[i] = ok ? r : -1;
+      col[i] = ok ? 8 * (pc ^ LY::flip(r)) : 0;
+    }
   }
-}
+  __device__ __forceinline__ void issue(uint16_t* lds, const uint16_t* __restrict__ g, long long row_stride, int row0,
+                                        int rmax, int wave, int nw) const {
+#pragma unroll
+    for (int i = 0; i < MAXI; ++i) {
+      const int n = wave + i * nw;
+      if (n < NI && row[i] >= 0) {
+        const int gr = min(row0 + row[i], rmax);
+        __builtin_amdgcn_global_load_lds(g + gr * row_stride + col[i], (lds_void*)(lds + n * kWave * 8), 16, 0, 0);
+      }
+    }
+  }
+};
 
 // 64 consecutive 4-byte values (clamped at index imax) into LDS, by one wave.
 __device__ __forceinline__ void stage_words(void* lds, const void* __restrict__ g, int i0, int imax, int lane) {

@@ -173,12 +173,13 @@ __device__ __forceinline__ int walker_next(TileWalker& w, const int2* __restrict
 
 // ---------------------------------------------------------------- operand reads from swizzled tiles
 // S^T block (32 keys x 32 queries) of the current tile: A = K rows from LDS, B = Q^T in registers.
+// rl = Lay<D>::row_lane(lane).
 template <int D>
-__device__ __forceinline__ f32x16 scores_t(const uint16_t* tile, int row0, const bf16x8* breg, int col, int half) {
+__device__ __forceinline__ f32x16 scores_t(const uint16_t* tile, int row0, const bf16x8* breg, int rl) {
   f32x16 s = {};
-  const int r = row0 + col;
+  const uint16_t* base = tile + rl + row0 * Lay<D>::PITCH;
 #pragma unroll
-  for (int ks = 0; ks < D / 16; ++ks) s = mfma32(lds_read_b128(tile + Swz<D>::off(r, 16 * ks + 8 * half)), breg[ks], s);
+  for (int ks = 0; ks < D / 16; ++ks) s = mfma32(lds_read_b128(base + 16 * ks), breg[ks], s);
   return s;
 }
 
@@ -199,18 +200,14 @@ __device__ __forceinline__ void mask_t(f32x16& s, const int* sE, int kb, int j0,
   }
 }
 
-// A operand of a 32x32x16 MFMA read transposed from a swizzled tile: rows
-// (contraction index) r0 + {0..3} and r0 + 8 + {0..3} with r0 = row0 + 4 half
+// A operand of a 32x32x16 MFMA read transposed from an LDS tile: rows
+// (contraction index) row0 + 4 half + {0..3} and row0 + 8 + 4 half + {0..3}
 // (the order in which the C layout of a score block lists its 16 values),
-// columns c0 + (l % 32).
+// columns c0 + (l % 32).  tl, th = Lay<D>::tr_lo(lane), tr_hi(lane).
 template <int D>
-__device__ __forceinline__ bf16x8 tr_operand(const uint16_t* tile, int row0, int c0, int lane) {
-  const int li = lane & 15, g16 = lane >> 4;
-  const int r = row0 + 4 * (g16 >> 1) + (li >> 2);
-  const int c = c0 + 16 * (g16 & 1) + 4 * (li & 3);
-  const s16x4 lo = lds_read_tr(tile + Swz<D>::off(r, c));
-  const s16x4 hi = lds_read_tr(tile + Swz<D>::off(r + 8, c));
-  return cat_tr(lo, hi);
+__device__ __forceinline__ bf16x8 tr_operand(const uint16_t* tile, int row0, int c0, int tl, int th) {
+  const int o = row0 * Lay<D>::PITCH + c0;
+  return cat_tr(lds_read_tr(tile + tl + o), lds_read_tr(tile + th + o));
 }
 
 // Head grouping of a row-kernel workgroup.
@@ -242,13 +239,16 @@ __device__ __forceinline__ bool row_tile(const RowArgs& a, RowTile& t) {
 
 // Asynchronous staging of one 64-key K/V (and evict_at) tile of KV head g.
 template <int D>
-__device__ __forceinline__ void stage_kv(uint16_t* sK, uint16_t* sV, int* sE, const RowArgs& a, const RowTile& rt,
-                                         int kt, int wave, int nw, int lane) {
+using KVStager = RowStager<D, kKeyTile, (kKeyTile * Lay<D>::CPRP / kWave + 3) / 4>;   // >= 4 waves
+
+template <int D>
+__device__ __forceinline__ void stage_kv(const KVStager<D>& st, uint16_t* sK, uint16_t* sV, int* sE, const RowArgs& a,
+                                         const RowTile& rt, int kt, int wave, int nw, int lane) {
   const int j0 = kt * kKeyTile;
   const long long base = ((long long)rt.tr.tok0 * a.Hkv + rt.g) * D;
   const long long stride = (long long)a.Hkv * D;
-  stage_rows<D, kKeyTile>(sK, a.k + base, stride, j0, rt.tr.L - 1, wave, nw, lane);
-  stage_rows<D, kKeyTile>(sV, a.v + base, stride, j0, rt.tr.L - 1, wave, nw, lane);
+  st.issue(sK, a.k + base, stride, j0, rt.tr.L - 1, wave, nw);
+  st.issue(sV, a.v + base, stride, j0, rt.tr.L - 1, wave, nw);
   if (wave == nw - 1) stage_words(sE, a.evict + rt.tr.tok0, j0, rt.tr.L - 1, lane);
 }
 
@@ -260,10 +260,10 @@ __device__ __forceinline__ void stage_kv(uint16_t* sK, uint16_t* sV, int* sE, co
 template <int D>
 __global__ void __launch_bounds__(512) fwd_kernel(RowArgs a) {
   constexpr int KS = D / 16, DB = D / 32;
-  __shared__ __attribute__((aligned(1024))) uint16_t sK0[kKeyTile * D];
-  __shared__ __attribute__((aligned(1024))) uint16_t sK1[kKeyTile * D];
-  __shared__ __attribute__((aligned(1024))) uint16_t sV0[kKeyTile * D];
-  __shared__ __attribute__((aligned(1024))) uint16_t sV1[kKeyTile * D];
+  __shared__ __attribute__((aligned(1024))) uint16_t sK0[kKeyTile * Lay<D>::PITCH];
+  __shared__ __attribute__((aligned(1024))) uint16_t sK1[kKeyTile * Lay<D>::PITCH];
+  __shared__ __attribute__((aligned(1024))) uint16_t sV0[kKeyTile * Lay<D>::PITCH];
+  __shared__ __attribute__((aligned(1024))) uint16_t sV1[kKeyTile * Lay<D>::PITCH];
   __shared__ __attribute__((aligned(256))) int sE0[kKeyTile];
   __shared__ __attribute__((aligned(256))) int sE1[kKeyTile];
 
@@ -274,6 +274,9 @@ __global__ void __launch_bounds__(512) fwd_kernel(RowArgs a) {
   const Trace tr = rt.tr;
   const int i = rt.i0w + col;
   const bool row_ok = i < tr.L;
+  const int rl = Lay<D>::row_lane(lane), tl = Lay<D>::tr_lo(lane), th = Lay<D>::tr_hi(lane);
+  KVStager<D> kvst;
+  kvst.init(wave, nw, lane);
 
   bf16x8 qreg[KS];
   {
@@ -301,7 +304,7 @@ __global__ void __launch_bounds__(512) fwd_kernel(RowArgs a) {
     int2 nkst = make_int2(0, 0);
     if (nkt >= 0) {
       nkst = a.kstats[kidx0 + nkt];
-      stage_kv<D>(nK, nV, nE, a, rt, nkt, wave, nw, lane);
+      stage_kv<D>(kvst, nK, nV, nE, a, rt, nkt, wave, nw, lane);
     }
     const int j0 = kt * kKeyTile;
     const int cls = tile_class(rt.i0w, rt.i0w + 32, j0, j0 + kKeyTile, tr.L, kst.x, kst.y);
@@ -309,7 +312,7 @@ __global__ void __launch_bounds__(512) fwd_kernel(RowArgs a) {
       f32x16 s[2];
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
-        s[kb] = scores_t<D>(cK, 32 * kb, qreg, col, half);
+        s[kb] = scores_t<D>(cK, 32 * kb, qreg, rl);
         if (cls == kPartial) mask_t(s[kb], cE, kb, j0, i, tr.L, half);
       }
       float mx = -INFINITY;
@@ -345,7 +348,7 @@ __global__ void __launch_bounds__(512) fwd_kernel(RowArgs a) {
           const bf16x8 pb = pack8(s[kb], 8 * t);
 #pragma unroll
           for (int d = 0; d < DB; ++d)
-            acc[d] = mfma32(tr_operand<D>(cV, 32 * kb + 16 * t, 32 * d, lane), pb, acc[d]);
+            acc[d] = mfma32(tr_operand<D>(cV, 32 * kb + 16 * t, 32 * d, tl, th), pb, acc[d]);
         }
     }
     wait_vm();
@@ -354,7 +357,7 @@ __global__ void __launch_bounds__(512) fwd_kernel(RowArgs a) {
     kst = nkst;
   };
 
-  if (kt >= 0) stage_kv<D>(sK0, sV0, sE0, a, rt, kt, wave, nw, lane);
+  if (kt >= 0) stage_kv<D>(kvst, sK0, sV0, sE0, a, rt, kt, wave, nw, lane);
   wait_vm();
   __syncthreads();
   while (kt >= 0) {
@@ -381,10 +384,11 @@ __global__ void __launch_bounds__(512) fwd_kernel(RowArgs a) {
 }
 
 // ---------------------------------------------------------------- backward: Delta = rowsum(dO * O)
+// Also writes LSE * log2(e), the form in which the backward kernels use it.
 template <int D>
 __global__ void __launch_bounds__(256) bwd_pre_kernel(const uint16_t* __restrict__ o, const uint16_t* __restrict__ dout,
-                                                      float* __restrict__ delta, int ntok, int Hq, int T,
-                                                      int varlen) {
+                                                      const float* __restrict__ lse, float* __restrict__ delta,
+                                                      float* __restrict__ lse2, int ntok, int Hq, int T, int varlen) {
   constexpr int PER = D / 16;  // elements per lane, 16 lanes per row
   const int sub = threadIdx.x & 15;
   const long long row = (long long)blockIdx.x * (blockDim.x / 16) + (threadIdx.x >> 4);
@@ -405,6 +409,7 @@ __global__ void __launch_bounds__(256) bwd_pre_kernel(const uint16_t* __restrict
     const int tok = (int)(row / Hq), h = (int)(row % Hq);
     const long long idx = varlen ? (long long)h * ntok + tok : ((long long)(tok / T) * Hq + h) * T + tok % T;
     delta[idx] = s;
+    lse2[idx] = lse[idx] * 1.4426950408889634f;
   }
 }
 
@@ -412,10 +417,10 @@ __global__ void __launch_bounds__(256) bwd_pre_kernel(const uint16_t* __restrict
 template <int D>
 __global__ void __launch_bounds__(512) dq_kernel(RowArgs a) {
   constexpr int KS = D / 16, DB = D / 32;
-  __shared__ __attribute__((aligned(1024))) uint16_t sK0[kKeyTile * D];
-  __shared__ __attribute__((aligned(1024))) uint16_t sK1[kKeyTile * D];
-  __shared__ __attribute__((aligned(1024))) uint16_t sV0[kKeyTile * D];
-  __shared__ __attribute__((aligned(1024))) uint16_t sV1[kKeyTile * D];
+  __shared__ __attribute__((aligned(1024))) uint16_t sK0[kKeyTile * Lay<D>::PITCH];
+  __shared__ __attribute__((aligned(1024))) uint16_t sK1[kKeyTile * Lay<D>::PITCH];
+  __shared__ __attribute__((aligned(1024))) uint16_t sV0[kKeyTile * Lay<D>::PITCH];
+  __shared__ __attribute__((aligned(1024))) uint16_t sV1[kKeyTile * Lay<D>::PITCH];
   __shared__ __attribute__((aligned(256))) int sE0[kKeyTile];
   __shared__ __attribute__((aligned(256))) int sE1[kKeyTile];
 
@@ -426,6 +431,9 @@ __global__ void __launch_bounds__(512) dq_kernel(RowArgs a) {
   const Trace tr = rt.tr;
   const int i = rt.i0w + col;
   const bool row_ok = i < tr.L;
+  const int rl = Lay<D>::row_lane(lane), tl = Lay<D>::tr_lo(lane), th = Lay<D>::tr_hi(lane);
+  KVStager<D> kvst;
+  kvst.init(wave, nw, lane);
   const int ic = min(i, tr.L - 1);
 
   bf16x8 qreg[KS], oreg[KS];
@@ -438,7 +446,7 @@ __global__ void __launch_bounds__(512) dq_kernel(RowArgs a) {
       oreg[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(a.dout + roff + 16 * ks));
     }
     const long long li = lse_index(a.varlen, a.ntok, a.Hq, a.T, rt.b, rt.h, tr.tok0, ic);
-    lse2 = a.lse_in[li] * 1.4426950408889634f;
+    lse2 = a.lse_in[li];   // already scaled by log2(e)
     dlt = a.delta[li];
   }
 
@@ -459,16 +467,16 @@ __global__ void __launch_bounds__(512) dq_kernel(RowArgs a) {
     int2 nkst = make_int2(0, 0);
     if (nkt >= 0) {
       nkst = a.kstats[kidx0 + nkt];
-      stage_kv<D>(nK, nV, nE, a, rt, nkt, wave, nw, lane);
+      stage_kv<D>(kvst, nK, nV, nE, a, rt, nkt, wave, nw, lane);
     }
     const int j0 = kt * kKeyTile;
     const int cls = tile_class(rt.i0w, rt.i0w + 32, j0, j0 + kKeyTile, tr.L, kst.x, kst.y);
     if (cls != kEmpty) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
-        f32x16 s = scores_t<D>(cK, 32 * kb, qreg, col, half);
+        f32x16 s = scores_t<D>(cK, 32 * kb, qreg, rl);
         if (cls == kPartial) mask_t(s, cE, kb, j0, i, tr.L, half);
-        const f32x16 dp = scores_t<D>(cV, 32 * kb, oreg, col, half);
+        const f32x16 dp = scores_t<D>(cV, 32 * kb, oreg, rl);
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], a.scale_log2, -lse2));
@@ -479,7 +487,7 @@ __global__ void __launch_bounds__(512) dq_kernel(RowArgs a) {
           const bf16x8 dsb = pack8(s, 8 * t);
 #pragma unroll
           for (int d = 0; d < DB; ++d)
-            acc[d] = mfma32(tr_operand<D>(cK, 32 * kb + 16 * t, 32 * d, lane), dsb, acc[d]);
+            acc[d] = mfma32(tr_operand<D>(cK, 32 * kb + 16 * t, 32 * d, tl, th), dsb, acc[d]);
         }
       }
     }
@@ -489,7 +497,7 @@ __global__ void __launch_bounds__(512) dq_kernel(RowArgs a) {
     kst = nkst;
   };
 
-  if (kt >= 0) stage_kv<D>(sK0, sV0, sE0, a, rt, kt, wave, nw, lane);
+  if (kt >= 0) stage_kv<D>(kvst, sK0, sV0, sE0, a, rt, kt, wave, nw, lane);
   wait_vm();
   __syncthreads();
   while (kt >= 0) {
@@ -512,13 +520,22 @@ __global__ void __launch_bounds__(512) dq_kernel(RowArgs a) {
 }
 
 // ---------------------------------------------------------------- backward: dK, dV (column kernel)
+// One workgroup: 128 keys of one KV head, 8 waves.  Waves 0-3 accumulate dV
+// and waves 4-7 accumulate dK, each for 32 keys (wave w and w + 4 share the
+// same keys and run on the same SIMD).  Both read the Q / dO blocks staged
+// once in LDS for the workgroup; the dV waves compute S -> P -> dV^T += dO^T P,
+// the dK waves compute S, dP -> dS -> dK^T += Q^T dS.  S is computed by both
+// (one extra product per block) so each wave holds only one accumulator and
+// two waves fit on a SIMD.  The workgroup walks the query rows that can see
+// any of its keys in steps of 64 rows x one q-head of the group.  Masking is
+// branch-free: rows outside [j, min(e_j, L)) get P = 0.
 template <int D>
-__global__ void __launch_bounds__(256) dkdv_kernel(ColArgs a) {
-  constexpr int KS = D / 16, DB = D / 32;
-  __shared__ __attribute__((aligned(1024))) uint16_t sQ0[kQStep * D];
-  __shared__ __attribute__((aligned(1024))) uint16_t sQ1[kQStep * D];
-  __shared__ __attribute__((aligned(1024))) uint16_t sO0[kQStep * D];
-  __shared__ __attribute__((aligned(1024))) uint16_t sO1[kQStep * D];
+__global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) dkdv_kernel(ColArgs a) {
+  constexpr int KS = D / 16, DB = D / 32, PITCH = Lay<D>::PITCH;
+  __shared__ __attribute__((aligned(1024))) uint16_t sQ0[kQStep * PITCH];
+  __shared__ __attribute__((aligned(1024))) uint16_t sQ1[kQStep * PITCH];
+  __shared__ __attribute__((aligned(1024))) uint16_t sO0[kQStep * PITCH];
+  __shared__ __attribute__((aligned(1024))) uint16_t sO1[kQStep * PITCH];
   __shared__ __attribute__((aligned(256))) float sL0[kQStep];
   __shared__ __attribute__((aligned(256))) float sL1[kQStep];
   __shared__ __attribute__((aligned(256))) float sD0[kQStep];
@@ -536,19 +553,24 @@ __global__ void __launch_bounds__(256) dkdv_kernel(ColArgs a) {
   if (j0 >= tr.L) return;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const bool role_dk = wave >= 4;
+  const int kw = wave & 3;
   const int half = lane >> 5, col = lane & 31;
-  const int jw0 = j0 + 32 * wave;
-  const int j = jw0 + col;
+  const int j = j0 + 32 * kw + col;
   const bool key_ok = j < tr.L;
   const int jc = min(j, tr.L - 1);
   const int ej = key_ok ? min(a.evict[tr.tok0 + j], tr.L) : 0;
+  const unsigned kspan = key_ok ? (unsigned)(ej - j) : 0u;   // rows j .. ej - 1 see this key
+  const int rl = Lay<D>::row_lane(lane), tl = Lay<D>::tr_lo(lane), th = Lay<D>::tr_hi(lane);
   int emin_w = key_ok ? ej : INT_MAX, emax_w = key_ok ? ej : INT_MIN;
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) {
     emin_w = min(emin_w, __shfl_xor(emin_w, off));
     emax_w = max(emax_w, __shfl_xor(emax_w, off));
   }
-  if (lane == 0) sEmax[wave] = emax_w;
+  if (!role_dk && lane == 0) sEmax[kw] = emax_w;
+  RowStager<D, kQStep, 3> qst;
+  qst.init(wave, 8, lane);
 
   bf16x8 kreg[KS], vreg[KS];
   {
@@ -556,7 +578,7 @@ __global__ void __launch_bounds__(256) dkdv_kernel(ColArgs a) {
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       kreg[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(a.k + koff + 16 * ks));
-      vreg[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(a.v + koff + 16 * ks));
+      vreg[ks] = role_dk ? as_bf16x8(*reinterpret_cast<const uint4*>(a.v + koff + 16 * ks)) : bf16x8{};
     }
   }
   __syncthreads();
@@ -565,26 +587,22 @@ __global__ void __launch_bounds__(256) dkdv_kernel(ColArgs a) {
   const int qs_hi = (emax_wg + kQStep - 1) / kQStep;
   const int steps = (qs_hi - qs_lo) * a.G;
 
-  f32x16 dk[DB], dv[DB];
+  f32x16 acc[DB];   // dV^T (waves 0-3) or dK^T (waves 4-7): rows d, column = this lane's key
 #pragma unroll
-  for (int d = 0; d < DB; ++d) {
-    dk[d] = f32x16{};
-    dv[d] = f32x16{};
-  }
+  for (int d = 0; d < DB; ++d) acc[d] = f32x16{};
 
   auto stage = [&](uint16_t* q_, uint16_t* o_, float* l_, float* d_, int step) {
     const int i0 = (qs_lo + step / a.G) * kQStep;
     const int h = g * a.G + step % a.G;
     const long long base = ((long long)tr.tok0 * a.Hq + h) * D;
-    stage_rows<D, kQStep>(q_, a.q + base, (long long)a.Hq * D, i0, tr.L - 1, wave, 4, lane);
-    stage_rows<D, kQStep>(o_, a.dout + base, (long long)a.Hq * D, i0, tr.L - 1, wave, 4, lane);
+    qst.issue(q_, a.q + base, (long long)a.Hq * D, i0, tr.L - 1, wave, 8);
+    qst.issue(o_, a.dout + base, (long long)a.Hq * D, i0, tr.L - 1, wave, 8);
     const long long lb = lse_index(a.varlen, a.ntok, a.Hq, a.T, b, h, tr.tok0, 0);
-    if (wave == 0) stage_words(l_, a.lse + lb, i0, tr.L - 1, lane);
-    if (wave == 1) stage_words(d_, a.delta + lb, i0, tr.L - 1, lane);
+    if (wave == 6) stage_words(l_, a.lse + lb, i0, tr.L - 1, lane);   // LSE * log2(e)
+    if (wave == 7) stage_words(d_, a.delta + lb, i0, tr.L - 1, lane);
   };
 
   int step = 0;
-  // One step: prefetch step + 1 into the other buffers, compute on (cQ, cO, cL, cD).
   auto body = [&](const uint16_t* cQ, const uint16_t* cO, const float* cL, const float* cD, uint16_t* nQ,
                   uint16_t* nO, float* nL, float* nD) {
     if (step + 1 < steps) stage(nQ, nO, nL, nD, step + 1);
@@ -592,45 +610,54 @@ __global__ void __launch_bounds__(256) dkdv_kernel(ColArgs a) {
 #pragma unroll
     for (int sb = 0; sb < kQStep / 32; ++sb) {
       const int ib = i0 + 32 * sb;
+      const int jw0 = j0 + 32 * kw;
       const int cls = tile_class(ib, ib + 32, jw0, jw0 + 32, tr.L, emin_w, emax_w);
       if (cls == kEmpty) continue;
-      // S = Q K^T and dP = dO V^T for 32 rows x this wave's 32 keys (C layout: lane <-> key).
-      f32x16 s = {}, dp = {};
+      // S = Q K^T for 32 rows x this wave's 32 keys (C layout: lane <-> key,
+      // element r <-> row ib + 8 (r/4) + 4 half + r%4).
+      f32x16 x = {};
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const int o = Swz<D>::off(32 * sb + col, 16 * ks + 8 * half);
-        s = mfma32(lds_read_b128(cQ + o), kreg[ks], s);
-        dp = mfma32(lds_read_b128(cO + o), vreg[ks], dp);
-      }
-      f32x16 p, ds;
+      for (int ks = 0; ks < KS; ++ks) x = mfma32(lds_read_b128(cQ + rl + 32 * sb * PITCH + 16 * ks), kreg[ks], x);
+      // P = exp(s - LSE), in place; rows outside [j, min(e_j, L)) of a PARTIAL block get 0
 #pragma unroll
       for (int q4 = 0; q4 < 4; ++q4) {
-        const int rr = 32 * sb + 8 * q4 + 4 * half;
-        const float4 l4 = *reinterpret_cast<const float4*>(cL + rr);
-        const float4 d4 = *reinterpret_cast<const float4*>(cD + rr);
+        const float4 l4 = *reinterpret_cast<const float4*>(cL + 32 * sb + 8 * q4 + 4 * half);
         const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
-        const float dv4[4] = {d4.x, d4.y, d4.z, d4.w};
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          const int r = 4 * q4 + t;
-          float x = __builtin_fmaf(s[r], a.scale_log2, -lv[t] * 1.4426950408889634f);
-          if (cls == kPartial) {
-            const int ii = ib + 8 * q4 + 4 * half + t;
-            if (!((j <= ii) && (ii < ej) && (ii < tr.L))) x = -INFINITY;
-          }
-          p[r] = __builtin_amdgcn_exp2f(x);
-          ds[r] = p[r] * (dp[r] - dv4[t]);
+        for (int t = 0; t < 4; ++t) x[4 * q4 + t] = __builtin_fmaf(x[4 * q4 + t], a.scale_log2, -lv[t]);
+      }
+      if (cls == kPartial) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const bool vis = (unsigned)(ib + 8 * (r >> 2) + 4 * half + (r & 3) - j) < kspan;
+          x[r] = vis ? x[r] : -INFINITY;
         }
       }
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        const bf16x8 pb = pack8(p, 8 * t);
-        const bf16x8 dsb = pack8(ds, 8 * t);
+      for (int r = 0; r < 16; ++r) x[r] = __builtin_amdgcn_exp2f(x[r]);
+      if (role_dk) {
+        // dS = P (dP - Delta): the dP accumulator starts at -Delta of its row
+        f32x16 dp;
 #pragma unroll
-        for (int d = 0; d < DB; ++d) {
-          dv[d] = mfma32(tr_operand<D>(cO, 32 * sb + 16 * t, 32 * d, lane), pb, dv[d]);
-          dk[d] = mfma32(tr_operand<D>(cQ, 32 * sb + 16 * t, 32 * d, lane), dsb, dk[d]);
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const float4 d4 = *reinterpret_cast<const float4*>(cD + 32 * sb + 8 * q4 + 4 * half);
+          dp[4 * q4] = -d4.x;
+          dp[4 * q4 + 1] = -d4.y;
+          dp[4 * q4 + 2] = -d4.z;
+          dp[4 * q4 + 3] = -d4.w;
         }
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) dp = mfma32(lds_read_b128(cO + rl + 32 * sb * PITCH + 16 * ks), vreg[ks], dp);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) x[r] *= dp[r];
+      }
+      // dV^T += dO^T P  or  dK^T += Q^T dS (A operand read transposed from the staged tile)
+      const uint16_t* src = role_dk ? cQ : cO;
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const bf16x8 xb = pack8(x, 8 * t);
+#pragma unroll
+        for (int d = 0; d < DB; ++d) acc[d] = mfma32(tr_operand<D>(src, 32 * sb + 16 * t, 32 * d, tl, th), xb, acc[d]);
       }
     }
     wait_vm();
@@ -649,19 +676,24 @@ __global__ void __launch_bounds__(256) dkdv_kernel(ColArgs a) {
 
   if (key_ok) {
     const size_t koff = ((size_t)(tr.tok0 + j) * a.Hkv + g) * D;
-    const float sc = a.scale;
+    uint16_t* dst = role_dk ? a.dk + koff : a.dv + koff;
+    const float sc = role_dk ? a.scale : 1.f;
 #pragma unroll
     for (int d = 0; d < DB; ++d)
 #pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        const int dd = 32 * d + 8 * q4 + 4 * half;
-        *reinterpret_cast<uint2*>(a.dk + koff + dd) =
-            pack4_bf16(dk[d][4 * q4] * sc, dk[d][4 * q4 + 1] * sc, dk[d][4 * q4 + 2] * sc, dk[d][4 * q4 + 3] * sc);
-        *reinterpret_cast<uint2*>(a.dv + koff + dd) =
-            pack4_bf16(dv[d][4 * q4], dv[d][4 * q4 + 1], dv[d][4 * q4 + 2], dv[d][4 * q4 + 3]);
-      }
+      for (int q4 = 0; q4 < 4; ++q4)
+        *reinterpret_cast<uint2*>(dst + 32 * d + 8 * q4 + 4 * half) =
+            pack4_bf16(acc[d][4 * q4] * sc, acc[d][4 * q4 + 1] * sc, acc[d][4 * q4 + 2] * sc, acc[d][4 * q4 + 3] * sc);
   }
 }
+
+// Explicit instantiations: every kernel the launchers use is emitted, with its host stub.
+template __global__ void fwd_kernel<64>(RowArgs);
+template __global__ void fwd_kernel<128>(RowArgs);
+template __global__ void dq_kernel<64>(RowArgs);
+template __global__ void dq_kernel<128>(RowArgs);
+template __global__ void dkdv_kernel<64>(ColArgs);
+template __global__ void dkdv_kernel<128>(ColArgs);
 
 // ---------------------------------------------------------------- launchers
 size_t ws_kstats_bytes(int B, int ntok) {
@@ -669,7 +701,9 @@ size_t ws_kstats_bytes(int B, int ntok) {
   return (n * sizeof(int2) + 255) & ~(size_t)255;
 }
 
-size_t ws_delta_bytes(int Hq, int ntok) { return ((size_t)Hq * ntok * sizeof(float) + 255) & ~(size_t)255; }
+// Delta followed by LSE * log2(e), each [Hq][ntok] (or [B][Hq][T]) fp32.
+size_t ws_delta_bytes(int Hq, int ntok) { return 2 * (((size_t)Hq * ntok * sizeof(float) + 255) & ~(size_t)255); }
+static size_t half_delta_bytes(int Hq, int ntok) { return ws_delta_bytes(Hq, ntok) / 2; }
 
 static RowArgs row_args(const Problem& p, const int2* kstats) {
   RowArgs a{};
@@ -721,14 +755,15 @@ hipError_t launch_fwd(const Problem& p, const int2* kstats) {
 
 hipError_t launch_bwd_pre(const Problem& p, float* delta) {
   const long long rows = (long long)p.ntok * p.Hq;
+  float* lse2 = (float*)((char*)delta + half_delta_bytes(p.Hq, p.ntok));
   dim3 grid((unsigned)((rows + 15) / 16)), block(256);
   prof_begin("bwd_pre", p.stream);
   if (p.D == 128)
     hipLaunchKernelGGL(bwd_pre_kernel<128>, grid, block, 0, p.stream, (const uint16_t*)p.o_in,
-                       (const uint16_t*)p.dout, delta, p.ntok, p.Hq, p.T, (int)(p.cu != nullptr));
+                       (const uint16_t*)p.dout, p.lse_in, delta, lse2, p.ntok, p.Hq, p.T, (int)(p.cu != nullptr));
   else
     hipLaunchKernelGGL(bwd_pre_kernel<64>, grid, block, 0, p.stream, (const uint16_t*)p.o_in,
-                       (const uint16_t*)p.dout, delta, p.ntok, p.Hq, p.T, (int)(p.cu != nullptr));
+                       (const uint16_t*)p.dout, p.lse_in, delta, lse2, p.ntok, p.Hq, p.T, (int)(p.cu != nullptr));
   prof_end(p.stream);
   return hipGetLastError();
 }
@@ -739,7 +774,7 @@ hipError_t launch_bwd_dkdv(const Problem& p, const float* delta) {
   a.k = (const uint16_t*)p.k;
   a.v = (const uint16_t*)p.v;
   a.dout = (const uint16_t*)p.dout;
-  a.lse = p.lse_in;
+  a.lse = (const float*)((const char*)delta + half_delta_bytes(p.Hq, p.ntok));   // LSE * log2(e)
   a.delta = delta;
   a.evict = p.evict;
   a.cu = p.cu;
@@ -757,8 +792,8 @@ hipError_t launch_bwd_dkdv(const Problem& p, const float* delta) {
   a.scale_log2 = p.scale * 1.4426950408889634f;
   const long long nblk = (long long)a.nkt * p.B * p.Hkv;
   prof_begin("bwd_dkdv", p.stream);
-  if (p.D == 128) hipLaunchKernelGGL(dkdv_kernel<128>, dim3((unsigned)nblk), dim3(256), 0, p.stream, a);
-  else hipLaunchKernelGGL(dkdv_kernel<64>, dim3((unsigned)nblk), dim3(256), 0, p.stream, a);
+  if (p.D == 128) hipLaunchKernelGGL(dkdv_kernel<128>, dim3((unsigned)nblk), dim3(512), 0, p.stream, a);
+  else hipLaunchKernelGGL(dkdv_kernel<64>, dim3((unsigned)nblk), dim3(512), 0, p.stream, a);
   prof_end(p.stream);
   return hipGetLastError();
 }
@@ -766,6 +801,7 @@ hipError_t launch_bwd_dkdv(const Problem& p, const float* delta) {
 hipError_t launch_bwd_dq(const Problem& p, const int2* kstats, const float* delta) {
   RowArgs a = row_args(p, kstats);
   a.delta = delta;
+  a.lse_in = (const float*)((const char*)delta + half_delta_bytes(p.Hq, p.ntok));   // LSE * log2(e)
   const long long nblk = (long long)a.nqt * p.B * p.Hkv * p.nhg;
   dim3 grid((unsigned)nblk), block(64 * p.HG * p.TC);
   prof_begin("bwd_dq", p.stream);
