@@ -52,7 +52,8 @@ kvs_status_t check_dims(int B, int T, long long ntok, int Hq, int Hkv, int D) {
 }
 
 // Workgroup shape of the row kernels: HG q-heads (largest divisor of G that
-// is <= 8) times TC chunks of 32 tokens, 4 to 8 waves in all.
+// is <= 8) times TC chunks of 32 tokens, 4 to 8 waves in all.  Two such
+// workgroups share a CU.
 void head_grouping(kvs::Problem& p) {
   int hg = 1;
   for (int d = 1; d <= 8; ++d)

@@ -158,6 +158,8 @@ struct RowStager {
       col[i] = ok ? 8 * (pc ^ LY::flip(r)) : 0;
     }
   }
+  // number of copy instructions one call of issue() makes for this wave
+  __device__ static __forceinline__ int count(int wave, int nw) { return wave < NI ? (NI - 1 - wave) / nw + 1 : 0; }
   __device__ __forceinline__ void issue(uint16_t* lds, const uint16_t* __restrict__ g, long long row_stride, int row0,
                                         int rmax, int wave, int nw) const {
 #pragma unroll
@@ -179,5 +181,18 @@ __device__ __forceinline__ void stage_words(void* lds, const void* __restrict__ 
 
 // Wait for this wave's outstanding global loads (including LDS-direct ones).
 __device__ __forceinline__ void wait_vm() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// Wait until at most n of this wave's vector memory operations are outstanding
+// (they complete in issue order, so everything issued before the last n is done).
+__device__ __forceinline__ void wait_vm_upto(int n) {
+  switch (n) {
+#define KVS_VM_CASE(k) case k: __builtin_amdgcn_s_waitcnt(0x0F70 | k); break;
+    KVS_VM_CASE(1) KVS_VM_CASE(2) KVS_VM_CASE(3) KVS_VM_CASE(4) KVS_VM_CASE(5) KVS_VM_CASE(6) KVS_VM_CASE(7)
+    KVS_VM_CASE(8) KVS_VM_CASE(9) KVS_VM_CASE(10) KVS_VM_CASE(11) KVS_VM_CASE(12) KVS_VM_CASE(13) KVS_VM_CASE(14)
+    KVS_VM_CASE(15)
+#undef KVS_VM_CASE
+    default: __builtin_amdgcn_s_waitcnt(0x0F70); break;
+  }
+}
 
 }  // namespace kvs

@@ -24,6 +24,7 @@
 #include "kvs_launch.h"
 
 #include <climits>
+#include <type_traits>
 
 namespace kvs {
 
@@ -321,9 +322,20 @@ __global__ void __launch_bounds__(512) fwd_kernel(RowArgs a) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
       mx = fmaxf(mx, wave_xor32(mx)) * a.scale_log2;
-      const float m_new = fmaxf(m_run, mx);
-      const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
+      // The reference max of a row only moves when the tile's max exceeds it by
+      // more than 8 (log2 units): probabilities are then at most 2^8, exact to
+      // rescale later, and the accumulator rescale is skipped for most tiles.
+      if (__ballot(mx > m_run + 8.f)) {
+        const float m_new = fmaxf(m_run, mx);
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);   // 0 on the first visible tile
+        l_run *= alpha;
+#pragma unroll
+        for (int d = 0; d < DB; ++d)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[d][r] *= alpha;
+        m_run = m_new;
+      }
+      const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
       float ls = 0.f;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
@@ -333,14 +345,7 @@ __global__ void __launch_bounds__(512) fwd_kernel(RowArgs a) {
           s[kb][r] = p;
           ls += p;
         }
-      l_run = l_run * alpha + ls;
-      m_run = m_new;
-      if (alpha != 1.f) {
-#pragma unroll
-        for (int d = 0; d < DB; ++d)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) acc[d][r] *= alpha;
-      }
+      l_run += ls;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -534,12 +539,16 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
   constexpr int KS = D / 16, DB = D / 32, PITCH = Lay<D>::PITCH;
   __shared__ __attribute__((aligned(1024))) uint16_t sQ0[kQStep * PITCH];
   __shared__ __attribute__((aligned(1024))) uint16_t sQ1[kQStep * PITCH];
+  __shared__ __attribute__((aligned(1024))) uint16_t sQ2[kQStep * PITCH];
   __shared__ __attribute__((aligned(1024))) uint16_t sO0[kQStep * PITCH];
   __shared__ __attribute__((aligned(1024))) uint16_t sO1[kQStep * PITCH];
+  __shared__ __attribute__((aligned(1024))) uint16_t sO2[kQStep * PITCH];
   __shared__ __attribute__((aligned(256))) float sL0[kQStep];
   __shared__ __attribute__((aligned(256))) float sL1[kQStep];
+  __shared__ __attribute__((aligned(256))) float sL2[kQStep];
   __shared__ __attribute__((aligned(256))) float sD0[kQStep];
   __shared__ __attribute__((aligned(256))) float sD1[kQStep];
+  __shared__ __attribute__((aligned(256))) float sD2[kQStep];
   __shared__ int sEmax[4];
 
   int wg = blockIdx.x;
@@ -602,77 +611,115 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
     if (wave == 7) stage_words(d_, a.delta + lb, i0, tr.L - 1, lane);
   };
 
-  int step = 0;
-  auto body = [&](const uint16_t* cQ, const uint16_t* cO, const float* cL, const float* cD, uint16_t* nQ,
-                  uint16_t* nO, float* nL, float* nD) {
-    if (step + 1 < steps) stage(nQ, nO, nL, nD, step + 1);
-    const int i0 = (qs_lo + step / a.G) * kQStep;
+  const int nissue = 2 * RowStager<D, kQStep, 3>::count(wave, 8) + (wave >= 6 ? 1 : 0);   // copies per step
+  const int jw0 = j0 + 32 * kw;
+
+  // One 32-row block: S = Q K^T (C layout: lane <-> key, element r <-> row
+  // rb + 8 (r/4) + 4 half + r%4 of the staged tile), then P = exp(s - LSE)
+  // (masked when `partial`), and for dK waves dS = P (dP - Delta) with the dP
+  // accumulator started at -Delta.  Returns P or dS in x.
+  auto block_s = [&](auto dk_tag, const uint16_t* cQ, const uint16_t* cO, const float* cL, const float* cD, int rb,
+                     int ib, bool partial, f32x16& x) {
+    constexpr bool DK = decltype(dk_tag)::value;
+    x = f32x16{};
 #pragma unroll
-    for (int sb = 0; sb < kQStep / 32; ++sb) {
-      const int ib = i0 + 32 * sb;
-      const int jw0 = j0 + 32 * kw;
-      const int cls = tile_class(ib, ib + 32, jw0, jw0 + 32, tr.L, emin_w, emax_w);
-      if (cls == kEmpty) continue;
-      // S = Q K^T for 32 rows x this wave's 32 keys (C layout: lane <-> key,
-      // element r <-> row ib + 8 (r/4) + 4 half + r%4).
-      f32x16 x = {};
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) x = mfma32(lds_read_b128(cQ + rl + 32 * sb * PITCH + 16 * ks), kreg[ks], x);
-      // P = exp(s - LSE), in place; rows outside [j, min(e_j, L)) of a PARTIAL block get 0
+    for (int ks = 0; ks < KS; ++ks) x = mfma32(lds_read_b128(cQ + rl + rb * PITCH + 16 * ks), kreg[ks], x);
+    f32x16 dp;
+    if (DK) {
 #pragma unroll
       for (int q4 = 0; q4 < 4; ++q4) {
-        const float4 l4 = *reinterpret_cast<const float4*>(cL + 32 * sb + 8 * q4 + 4 * half);
-        const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
-#pragma unroll
-        for (int t = 0; t < 4; ++t) x[4 * q4 + t] = __builtin_fmaf(x[4 * q4 + t], a.scale_log2, -lv[t]);
-      }
-      if (cls == kPartial) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const bool vis = (unsigned)(ib + 8 * (r >> 2) + 4 * half + (r & 3) - j) < kspan;
-          x[r] = vis ? x[r] : -INFINITY;
-        }
+        const float4 d4 = *reinterpret_cast<const float4*>(cD + rb + 8 * q4 + 4 * half);
+        dp[4 * q4] = -d4.x;
+        dp[4 * q4 + 1] = -d4.y;
+        dp[4 * q4 + 2] = -d4.z;
+        dp[4 * q4 + 3] = -d4.w;
       }
 #pragma unroll
-      for (int r = 0; r < 16; ++r) x[r] = __builtin_amdgcn_exp2f(x[r]);
-      if (role_dk) {
-        // dS = P (dP - Delta): the dP accumulator starts at -Delta of its row
-        f32x16 dp;
+      for (int ks = 0; ks < KS; ++ks) dp = mfma32(lds_read_b128(cO + rl + rb * PITCH + 16 * ks), vreg[ks], dp);
+    }
 #pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-          const float4 d4 = *reinterpret_cast<const float4*>(cD + 32 * sb + 8 * q4 + 4 * half);
-          dp[4 * q4] = -d4.x;
-          dp[4 * q4 + 1] = -d4.y;
-          dp[4 * q4 + 2] = -d4.z;
-          dp[4 * q4 + 3] = -d4.w;
-        }
+    for (int q4 = 0; q4 < 4; ++q4) {
+      const float4 l4 = *reinterpret_cast<const float4*>(cL + rb + 8 * q4 + 4 * half);
+      const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) dp = mfma32(lds_read_b128(cO + rl + 32 * sb * PITCH + 16 * ks), vreg[ks], dp);
+      for (int t = 0; t < 4; ++t) x[4 * q4 + t] = __builtin_fmaf(x[4 * q4 + t], a.scale_log2, -lv[t]);
+    }
+    if (partial) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) x[r] *= dp[r];
-      }
-      // dV^T += dO^T P  or  dK^T += Q^T dS (A operand read transposed from the staged tile)
-      const uint16_t* src = role_dk ? cQ : cO;
-#pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        const bf16x8 xb = pack8(x, 8 * t);
-#pragma unroll
-        for (int d = 0; d < DB; ++d) acc[d] = mfma32(tr_operand<D>(src, 32 * sb + 16 * t, 32 * d, tl, th), xb, acc[d]);
+      for (int r = 0; r < 16; ++r) {
+        const bool vis = (unsigned)(ib + 8 * (r >> 2) + 4 * half + (r & 3) - j) < kspan;
+        x[r] = vis ? x[r] : -INFINITY;
       }
     }
-    wait_vm();
-    __syncthreads();
-    ++step;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) x[r] = __builtin_amdgcn_exp2f(x[r]);
+    if (DK) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) x[r] *= dp[r];
+    }
+  };
+  // acc += (dO^T or Q^T) x for one 32-row block (A operand read transposed from the staged tile)
+  auto block_acc = [&](const uint16_t* src, int rb, const f32x16& x) {
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const bf16x8 xb = pack8(x, 8 * t);
+#pragma unroll
+      for (int d = 0; d < DB; ++d) acc[d] = mfma32(tr_operand<D>(src, rb + 16 * t, 32 * d, tl, th), xb, acc[d]);
+    }
   };
 
-  if (steps > 0) stage(sQ0, sO0, sL0, sD0, 0);
-  wait_vm();
-  __syncthreads();
-  while (step < steps) {
-    body(sQ0, sO0, sL0, sD0, sQ1, sO1, sL1, sD1);
-    if (step >= steps) break;
-    body(sQ1, sO1, sL1, sD1, sQ0, sO0, sL0, sD0);
-  }
+  // The step loop, specialised per role so each step is straight-line code.
+  // When both 32-row blocks are FULL for this wave (the common case) they are
+  // written as one basic block so the products of one block overlap the
+  // softmax arithmetic of the other.
+  auto run = [&](auto dk_tag) {
+    constexpr bool DK = decltype(dk_tag)::value;
+    int step = 0;
+    auto body = [&](const uint16_t* cQ, const uint16_t* cO, const float* cL, const float* cD, uint16_t* fQ,
+                    uint16_t* fO, float* fL, float* fD) {
+      const bool ahead = step + 2 < steps;
+      if (ahead) stage(fQ, fO, fL, fD, step + 2);
+      const int i0 = (qs_lo + step / a.G) * kQStep;
+      const uint16_t* src = DK ? cQ : cO;
+      const int c0 = tile_class(i0, i0 + 32, jw0, jw0 + 32, tr.L, emin_w, emax_w);
+      const int c1 = tile_class(i0 + 32, i0 + 64, jw0, jw0 + 32, tr.L, emin_w, emax_w);
+      if (c0 == kFull && c1 == kFull) {
+        f32x16 x0, x1;
+        block_s(dk_tag, cQ, cO, cL, cD, 0, i0, false, x0);
+        block_s(dk_tag, cQ, cO, cL, cD, 32, i0 + 32, false, x1);
+        block_acc(src, 0, x0);
+        block_acc(src, 32, x1);
+      } else {
+        if (c0 != kEmpty) {
+          f32x16 x0;
+          block_s(dk_tag, cQ, cO, cL, cD, 0, i0, c0 == kPartial, x0);
+          block_acc(src, 0, x0);
+        }
+        if (c1 != kEmpty) {
+          f32x16 x1;
+          block_s(dk_tag, cQ, cO, cL, cD, 32, i0 + 32, c1 == kPartial, x1);
+          block_acc(src, 32, x1);
+        }
+      }
+      wait_vm_upto(ahead ? nissue : 0);   // step + 1 has landed; step + 2 may still be in flight
+      __syncthreads();
+      ++step;
+    };
+    // Three-stage ring: step s is computed while s + 1 is in flight and s + 2 is issued.
+    if (steps > 0) stage(sQ0, sO0, sL0, sD0, 0);
+    if (steps > 1) stage(sQ1, sO1, sL1, sD1, 1);
+    wait_vm_upto(steps > 1 ? nissue : 0);
+    __syncthreads();
+    while (step < steps) {
+      body(sQ0, sO0, sL0, sD0, sQ2, sO2, sL2, sD2);
+      if (step >= steps) break;
+      body(sQ1, sO1, sL1, sD1, sQ0, sO0, sL0, sD0);
+      if (step >= steps) break;
+      body(sQ2, sO2, sL2, sD2, sQ1, sO1, sL1, sD1);
+    }
+  };
+  if (role_dk) run(std::true_type{});
+  else run(std::false_type{});
 
   if (key_ok) {
     const size_t koff = ((size_t)(tr.tok0 + j) * a.Hkv + g) * D;
