@@ -14,7 +14,6 @@ timed on a bounded sample of the same workload ("cpu_baseline").
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu]
 """
 import argparse
-import hashlib
 import json
 import math
 import os
@@ -42,14 +41,6 @@ def visible_pairs(evict_at, lengths):
     return tot
 
 
-def kernel_source_hash():
-    h = hashlib.sha256()
-    for f in ("kvs_kernels.hip", "kvs_device.h"):
-        with open(os.path.join(ROOT, "paper_2609_35750_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
-    return h.hexdigest()[:16]
-
-
 def load_traffic(kernel, workload):
     """HBM bytes per launch from the committed counter summary, if it was taken
     on the current kernel source; else None."""
@@ -58,7 +49,9 @@ def load_traffic(kernel, workload):
         return None
     with open(path) as fh:
         rec = json.load(fh)
-    if rec.get("source_hash") != kernel_source_hash():
+    from paper_2609_35750_amd.traffic import kernel_source_hash
+
+    if rec.get("source_hash") != kernel_source_hash(ROOT):
         return None
     return rec.get("bytes_per_launch")
 
