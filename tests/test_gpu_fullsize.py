@@ -2,8 +2,13 @@
 benchmark times, compared with the fp64 checker at sampled positions.
 
 The expected values come from ``tests/golden/make_parity_fixtures.py`` (which
-runs only the checker, for the q-heads of KV head 0).  Bound: max |x - x*| <=
-2e-2 and relative L2 <= 1e-2 for O, dQ, dK, dV; LSE within 1e-3.  Whole-tensor
+runs only the checker, for the q-heads of KV head 0).  Bound: |x - x*| <=
+2e-2 * max(1, |x*|) per element and relative L2 <= 1e-2 for O, dQ, dK, dV;
+LSE within 1e-3 absolute.  The 16k workload's query is the N(0,1) tensor
+times 1/sqrt(D) (softmax scale 1); its dQ is compared per unit of that N(0,1)
+tensor, i.e. both sides times 1/sqrt(D) (the chain rule through the fixed
+prescale), which puts it on the same O(1) scale as the other workloads' dQ.
+Whole-tensor
 properties (finite everywhere, the norm of the group's outputs) hold at any size.
 """
 import os
@@ -51,11 +56,12 @@ def test_fullsize_sampled_parity(kvs, name):
     rows, keys = gold["rows"], gold["keys"]
     report = {}
     report["O"] = assert_close(f"{name}:O", to_f64(res["O"][rows, :G]), gold["O"])
-    report["dQ"] = assert_close(f"{name}:dQ", to_f64(res["dq"][rows, :G]), gold["dQ"])
+    qs = 1.0 / np.sqrt(wl.D) if wl.q_prescaled else 1.0
+    report["dQ"] = assert_close(f"{name}:dQ", qs * to_f64(res["dq"][rows, :G]), qs * gold["dQ"].astype(np.float64))
     report["dK"] = assert_close(f"{name}:dK", to_f64(res["dk"][keys, 0]), gold["dK"])
     report["dV"] = assert_close(f"{name}:dV", to_f64(res["dv"][keys, 0]), gold["dV"])
     report["LSE"] = assert_close(f"{name}:LSE", to_f64(res["LSE"][:G][:, rows]), gold["LSE"], max_abs=LSE_ABS,
-                                 rel_l2=1e-4)
+                                 rel_l2=1e-4, elementwise=False)
     # whole-tensor norms of KV group 0 (every row, every key) against the checker's
     for key, gkey, sl in (("O", "norm_O", (slice(None), slice(0, G))), ("dq", "norm_dQ", (slice(None), slice(0, G))),
                           ("dk", "norm_dK", (slice(None), slice(0, 1))), ("dv", "norm_dV", (slice(None), slice(0, 1)))):
