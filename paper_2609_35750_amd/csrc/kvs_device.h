@@ -8,6 +8,7 @@ namespace kvs {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef short s16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -138,13 +139,14 @@ struct Lay {
 // of every piece are computed once (init) so that issuing a tile costs a
 // clamp and an address per piece.  Row r of the tile comes from global row
 // min(row0 + r, rmax) (rows past the end of a trace repeat its last row;
-// callers mask them).
+// callers mask them).  Lanes whose slot is row padding copy the row's first
+// chunk into it (padding is never read), so no lane is switched off.
 template <int D, int R, int MAXI>
 struct RowStager {
   using LY = Lay<D>;
   static constexpr int NI = R * LY::CPRP / kWave;   // 64-slot pieces per tile
   static_assert(R * LY::CPRP % kWave == 0, "tile must fill whole 64-slot pieces");
-  int row[MAXI];   // tile row of this lane's slot, or -1 (padding or no piece)
+  int row[MAXI];   // tile row of this lane's slot, or -1 (no piece)
   int col[MAXI];   // element column of the slot's first element in the source row
 
   __device__ __forceinline__ void init(int wave, int nw, int lane) {
@@ -153,9 +155,8 @@ struct RowStager {
       const int n = wave + i * nw;
       const int q = n * kWave + lane;
       const int r = q / LY::CPRP, pc = q - r * LY::CPRP;
-      const bool ok = n < NI && pc < LY::CPR;
-      row[i] = ok ? r : -1;
-      col[i] = ok ? 8 * (pc ^ LY::flip(r)) : 0;
+      row[i] = n < NI ? r : -1;
+      col[i] = (n < NI && pc < LY::CPR) ? 8 * (pc ^ LY::flip(r)) : 0;
     }
   }
   // number of copy instructions one call of issue() makes for this wave
@@ -165,7 +166,7 @@ struct RowStager {
 #pragma unroll
     for (int i = 0; i < MAXI; ++i) {
       const int n = wave + i * nw;
-      if (n < NI && row[i] >= 0) {
+      if (n < NI) {
         const int gr = min(row0 + row[i], rmax);
         __builtin_amdgcn_global_load_lds(g + gr * row_stride + col[i], (lds_void*)(lds + n * kWave * 8), 16, 0, 0);
       }

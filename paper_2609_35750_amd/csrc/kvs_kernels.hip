@@ -525,15 +525,19 @@ __global__ void __launch_bounds__(512) dq_kernel(RowArgs a) {
 }
 
 // ---------------------------------------------------------------- backward: dK, dV (column kernel)
-// One workgroup: 128 keys of one KV head, 8 waves.  Waves 0-3 accumulate dV
-// and waves 4-7 accumulate dK, each for 32 keys (wave w and w + 4 share the
-// same keys and run on the same SIMD).  Both read the Q / dO blocks staged
-// once in LDS for the workgroup; the dV waves compute S -> P -> dV^T += dO^T P,
-// the dK waves compute S, dP -> dS -> dK^T += Q^T dS.  S is computed by both
-// (one extra product per block) so each wave holds only one accumulator and
-// two waves fit on a SIMD.  The workgroup walks the query rows that can see
-// any of its keys in steps of 64 rows x one q-head of the group.  Masking is
-// branch-free: rows outside [j, min(e_j, L)) get P = 0.
+// One workgroup: 128 keys of one KV head, 8 waves.  Wave w < 4 (the "dV
+// wave") and wave w + 4 (the "dK wave") own the same 32 keys and share a SIMD.
+// The workgroup walks the query rows that can see any of its keys in steps of
+// 64 rows x one q-head of the group; Q, dO, LSE and Delta of a step are staged
+// once in LDS for all eight waves.  Per 32-row block:
+//   dV wave:  S = Q K^T,  P = exp2(S * scale * log2 e - LSE * log2 e) (masked),
+//             P -> LDS (bf16),  dV^T += dO^T P
+//   dK wave:  dP = dO V^T - Delta,  dS = P dP  (P read back from LDS),
+//             dK^T += Q^T dS
+// The dV waves run one step ahead of the dK waves (P of step s is written
+// during step s - 1), so a single barrier per step orders the exchange, every
+// product is computed once, and the two waves of a SIMD issue the same number
+// of MFMAs.  Masking happens only in the dV wave (masked P = 0 gives dS = 0).
 template <int D>
 __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) dkdv_kernel(ColArgs a) {
   constexpr int KS = D / 16, DB = D / 32, PITCH = Lay<D>::PITCH;
@@ -549,6 +553,9 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
   __shared__ __attribute__((aligned(256))) float sD0[kQStep];
   __shared__ __attribute__((aligned(256))) float sD1[kQStep];
   __shared__ __attribute__((aligned(256))) float sD2[kQStep];
+  // P exchange: [step parity][key quarter][32-row block][half of the 16 values][lane], 8 fp16 each
+  // (P <= 1; fp16 keeps 3 more mantissa bits than bf16 for dS = P dP)
+  __shared__ __attribute__((aligned(1024))) f16x8 sP[2 * 4 * 2 * 2 * kWave];
   __shared__ int sEmax[4];
 
   int wg = blockIdx.x;
@@ -581,14 +588,13 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
   RowStager<D, kQStep, 3> qst;
   qst.init(wave, 8, lane);
 
-  bf16x8 kreg[KS], vreg[KS];
+  // K (dV waves) or V (dK waves) of this lane's key: the B operand of S or dP
+  bf16x8 kvreg[KS];
   {
     const size_t koff = ((size_t)(tr.tok0 + jc) * a.Hkv + g) * D + 8 * half;
+    const uint16_t* src = role_dk ? a.v : a.k;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      kreg[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(a.k + koff + 16 * ks));
-      vreg[ks] = role_dk ? as_bf16x8(*reinterpret_cast<const uint4*>(a.v + koff + 16 * ks)) : bf16x8{};
-    }
+    for (int ks = 0; ks < KS; ++ks) kvreg[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(src + koff + 16 * ks));
   }
   __syncthreads();
   const int emax_wg = max(max(sEmax[0], sEmax[1]), max(sEmax[2], sEmax[3]));
@@ -596,11 +602,11 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
   const int qs_hi = (emax_wg + kQStep - 1) / kQStep;
   const int steps = (qs_hi - qs_lo) * a.G;
 
-  f32x16 acc[DB];   // dV^T (waves 0-3) or dK^T (waves 4-7): rows d, column = this lane's key
+  f32x16 acc[DB];   // dV^T (dV waves) or dK^T (dK waves): rows d, column = this lane's key
 #pragma unroll
   for (int d = 0; d < DB; ++d) acc[d] = f32x16{};
 
-  auto stage = [&](uint16_t* q_, uint16_t* o_, float* l_, float* d_, int step) {
+  auto stage = [&](uint16_t* q_, uint16_t* o_, float* l_, float* d_, int step) __attribute__((always_inline)) {
     const int i0 = (qs_lo + step / a.G) * kQStep;
     const int h = g * a.G + step % a.G;
     const long long base = ((long long)tr.tok0 * a.Hq + h) * D;
@@ -610,33 +616,23 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
     if (wave == 6) stage_words(l_, a.lse + lb, i0, tr.L - 1, lane);   // LSE * log2(e)
     if (wave == 7) stage_words(d_, a.delta + lb, i0, tr.L - 1, lane);
   };
-
-  const int nissue = 2 * RowStager<D, kQStep, 3>::count(wave, 8) + (wave >= 6 ? 1 : 0);   // copies per step
   const int jw0 = j0 + 32 * kw;
+  auto xslot = [&](int step, int blk, int t) __attribute__((always_inline)) { return sP + ((((step & 1) * 4 + kw) * 2 + blk) * 2 + t) * kWave + lane; };
 
-  // One 32-row block: S = Q K^T (C layout: lane <-> key, element r <-> row
-  // rb + 8 (r/4) + 4 half + r%4 of the staged tile), then P = exp(s - LSE)
-  // (masked when `partial`), and for dK waves dS = P (dP - Delta) with the dP
-  // accumulator started at -Delta.  Returns P or dS in x.
-  auto block_s = [&](auto dk_tag, const uint16_t* cQ, const uint16_t* cO, const float* cL, const float* cD, int rb,
-                     int ib, bool partial, f32x16& x) {
-    constexpr bool DK = decltype(dk_tag)::value;
-    x = f32x16{};
+  // acc += (dO^T or Q^T) x for one 32-row block (A operand read transposed from the staged tile)
+  auto block_acc = [&](const uint16_t* src, int rb, const bf16x8 (&xb)[2]) __attribute__((always_inline)) {
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) x = mfma32(lds_read_b128(cQ + rl + rb * PITCH + 16 * ks), kreg[ks], x);
-    f32x16 dp;
-    if (DK) {
+    for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        const float4 d4 = *reinterpret_cast<const float4*>(cD + rb + 8 * q4 + 4 * half);
-        dp[4 * q4] = -d4.x;
-        dp[4 * q4 + 1] = -d4.y;
-        dp[4 * q4 + 2] = -d4.z;
-        dp[4 * q4 + 3] = -d4.w;
-      }
+      for (int d = 0; d < DB; ++d) acc[d] = mfma32(tr_operand<D>(src, rb + 16 * t, 32 * d, tl, th), xb[t], acc[d]);
+  };
+  // dV wave, one 32-row block: S = Q K^T (C layout: lane <-> key, element r <->
+  // row rb + 8 (r/4) + 4 half + r%4 of the staged tile), P, P -> LDS, dV^T += dO^T P.
+  auto dv_block_s = [&](const uint16_t* cQ, const float* cL, int rb, int ib, bool partial, bf16x8 (&pb)[2],
+                        f16x8 (&ph)[2]) __attribute__((always_inline)) {
+    f32x16 x = {};
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) dp = mfma32(lds_read_b128(cO + rl + rb * PITCH + 16 * ks), vreg[ks], dp);
-    }
+    for (int ks = 0; ks < KS; ++ks) x = mfma32(lds_read_b128(cQ + rl + rb * PITCH + 16 * ks), kvreg[ks], x);
 #pragma unroll
     for (int q4 = 0; q4 < 4; ++q4) {
       const float4 l4 = *reinterpret_cast<const float4*>(cL + rb + 8 * q4 + 4 * half);
@@ -653,69 +649,123 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
     }
 #pragma unroll
     for (int r = 0; r < 16; ++r) x[r] = __builtin_amdgcn_exp2f(x[r]);
-    if (DK) {
+    pb[0] = pack8(x, 0);
+    pb[1] = pack8(x, 8);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) x[r] *= dp[r];
+    for (int e = 0; e < 8; ++e) {
+      ph[0][e] = (_Float16)x[e];
+      ph[1][e] = (_Float16)x[8 + e];
     }
   };
-  // acc += (dO^T or Q^T) x for one 32-row block (A operand read transposed from the staged tile)
-  auto block_acc = [&](const uint16_t* src, int rb, const f32x16& x) {
+  // dK wave, one 32-row block: dP = dO V^T - Delta, dS = P dP with P from LDS.
+  auto dk_block_s = [&](const uint16_t* cO, const float* cD, int rb, const f16x8* xp0, const f16x8* xp1,
+                        bf16x8 (&sb)[2]) __attribute__((always_inline)) {
+    f32x16 dp;
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      const bf16x8 xb = pack8(x, 8 * t);
+    for (int q4 = 0; q4 < 4; ++q4) {
+      const float4 d4 = *reinterpret_cast<const float4*>(cD + rb + 8 * q4 + 4 * half);
+      dp[4 * q4] = -d4.x;
+      dp[4 * q4 + 1] = -d4.y;
+      dp[4 * q4 + 2] = -d4.z;
+      dp[4 * q4 + 3] = -d4.w;
+    }
 #pragma unroll
-      for (int d = 0; d < DB; ++d) acc[d] = mfma32(tr_operand<D>(src, rb + 16 * t, 32 * d, tl, th), xb, acc[d]);
+    for (int ks = 0; ks < KS; ++ks) dp = mfma32(lds_read_b128(cO + rl + rb * PITCH + 16 * ks), kvreg[ks], dp);
+    const f16x8 p0 = *xp0, p1 = *xp1;
+    f32x16 x;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      x[e] = (float)p0[e] * dp[e];
+      x[8 + e] = (float)p1[e] * dp[8 + e];
+    }
+    sb[0] = pack8(x, 0);
+    sb[1] = pack8(x, 8);
+  };
+
+  auto dv_step = [&](int step, const uint16_t* cQ, const uint16_t* cO, const float* cL) __attribute__((always_inline)) {
+    const int i0 = (qs_lo + step / a.G) * kQStep;
+    const int c0 = tile_class(i0, i0 + 32, jw0, jw0 + 32, tr.L, emin_w, emax_w);
+    const int c1 = tile_class(i0 + 32, i0 + 64, jw0, jw0 + 32, tr.L, emin_w, emax_w);
+    if (c0 == kFull && c1 == kFull) {
+      bf16x8 p0[2], p1[2];
+      f16x8 h0[2], h1[2];
+      dv_block_s(cQ, cL, 0, i0, false, p0, h0);
+      dv_block_s(cQ, cL, 32, i0 + 32, false, p1, h1);
+      *xslot(step, 0, 0) = h0[0];
+      *xslot(step, 0, 1) = h0[1];
+      *xslot(step, 1, 0) = h1[0];
+      *xslot(step, 1, 1) = h1[1];
+      block_acc(cO, 0, p0);
+      block_acc(cO, 32, p1);
+    } else {
+      if (c0 != kEmpty) {
+        bf16x8 p0[2];
+        f16x8 h0[2];
+        dv_block_s(cQ, cL, 0, i0, c0 == kPartial, p0, h0);
+        *xslot(step, 0, 0) = h0[0];
+        *xslot(step, 0, 1) = h0[1];
+        block_acc(cO, 0, p0);
+      }
+      if (c1 != kEmpty) {
+        bf16x8 p1[2];
+        f16x8 h1[2];
+        dv_block_s(cQ, cL, 32, i0 + 32, c1 == kPartial, p1, h1);
+        *xslot(step, 1, 0) = h1[0];
+        *xslot(step, 1, 1) = h1[1];
+        block_acc(cO, 32, p1);
+      }
+    }
+  };
+  auto dk_step = [&](int step, const uint16_t* cQ, const uint16_t* cO, const float* cD) __attribute__((always_inline)) {
+    const int i0 = (qs_lo + step / a.G) * kQStep;
+    const int c0 = tile_class(i0, i0 + 32, jw0, jw0 + 32, tr.L, emin_w, emax_w);
+    const int c1 = tile_class(i0 + 32, i0 + 64, jw0, jw0 + 32, tr.L, emin_w, emax_w);
+    if (c0 != kEmpty && c1 != kEmpty) {
+      bf16x8 s0[2], s1[2];
+      dk_block_s(cO, cD, 0, xslot(step, 0, 0), xslot(step, 0, 1), s0);
+      dk_block_s(cO, cD, 32, xslot(step, 1, 0), xslot(step, 1, 1), s1);
+      block_acc(cQ, 0, s0);
+      block_acc(cQ, 32, s1);
+    } else {
+      if (c0 != kEmpty) {
+        bf16x8 s0[2];
+        dk_block_s(cO, cD, 0, xslot(step, 0, 0), xslot(step, 0, 1), s0);
+        block_acc(cQ, 0, s0);
+      }
+      if (c1 != kEmpty) {
+        bf16x8 s1[2];
+        dk_block_s(cO, cD, 32, xslot(step, 1, 0), xslot(step, 1, 1), s1);
+        block_acc(cQ, 32, s1);
+      }
     }
   };
 
-  // The step loop, specialised per role so each step is straight-line code.
-  // When both 32-row blocks are FULL for this wave (the common case) they are
-  // written as one basic block so the products of one block overlap the
-  // softmax arithmetic of the other.
-  auto run = [&](auto dk_tag) {
+  // Three-stage ring: during step s the dK waves read tile s, the dV waves tile
+  // s + 1, and tile s + 2 is copied into the buffer tile s - 1 used.
+  auto run = [&](auto dk_tag) __attribute__((always_inline)) {
     constexpr bool DK = decltype(dk_tag)::value;
     int step = 0;
-    auto body = [&](const uint16_t* cQ, const uint16_t* cO, const float* cL, const float* cD, uint16_t* fQ,
-                    uint16_t* fO, float* fL, float* fD) {
-      const bool ahead = step + 2 < steps;
-      if (ahead) stage(fQ, fO, fL, fD, step + 2);
-      const int i0 = (qs_lo + step / a.G) * kQStep;
-      const uint16_t* src = DK ? cQ : cO;
-      const int c0 = tile_class(i0, i0 + 32, jw0, jw0 + 32, tr.L, emin_w, emax_w);
-      const int c1 = tile_class(i0 + 32, i0 + 64, jw0, jw0 + 32, tr.L, emin_w, emax_w);
-      if (c0 == kFull && c1 == kFull) {
-        f32x16 x0, x1;
-        block_s(dk_tag, cQ, cO, cL, cD, 0, i0, false, x0);
-        block_s(dk_tag, cQ, cO, cL, cD, 32, i0 + 32, false, x1);
-        block_acc(src, 0, x0);
-        block_acc(src, 32, x1);
-      } else {
-        if (c0 != kEmpty) {
-          f32x16 x0;
-          block_s(dk_tag, cQ, cO, cL, cD, 0, i0, c0 == kPartial, x0);
-          block_acc(src, 0, x0);
-        }
-        if (c1 != kEmpty) {
-          f32x16 x1;
-          block_s(dk_tag, cQ, cO, cL, cD, 32, i0 + 32, c1 == kPartial, x1);
-          block_acc(src, 32, x1);
-        }
-      }
-      wait_vm_upto(ahead ? nissue : 0);   // step + 1 has landed; step + 2 may still be in flight
+    auto body = [&](const uint16_t* cQ, const uint16_t* cO, const float* cD, const uint16_t* nQ, const uint16_t* nO,
+                    const float* nL, uint16_t* zQ, uint16_t* zO, float* zL, float* zD) __attribute__((always_inline)) {
+      if (step + 2 < steps) stage(zQ, zO, zL, zD, step + 2);
+      if (DK) dk_step(step, cQ, cO, cD);
+      else if (step + 1 < steps) dv_step(step + 1, nQ, nO, nL);
+      wait_vm();   // tile step + 2 has landed (the dV waves read it next step)
       __syncthreads();
       ++step;
     };
-    // Three-stage ring: step s is computed while s + 1 is in flight and s + 2 is issued.
     if (steps > 0) stage(sQ0, sO0, sL0, sD0, 0);
     if (steps > 1) stage(sQ1, sO1, sL1, sD1, 1);
-    wait_vm_upto(steps > 1 ? nissue : 0);
+    wait_vm();
+    __syncthreads();
+    if (!DK && steps > 0) dv_step(0, sQ0, sO0, sL0);
     __syncthreads();
     while (step < steps) {
-      body(sQ0, sO0, sL0, sD0, sQ2, sO2, sL2, sD2);
+      body(sQ0, sO0, sD0, sQ1, sO1, sL1, sQ2, sO2, sL2, sD2);
       if (step >= steps) break;
-      body(sQ1, sO1, sL1, sD1, sQ0, sO0, sL0, sD0);
+      body(sQ1, sO1, sD1, sQ2, sO2, sL2, sQ0, sO0, sL0, sD0);
       if (step >= steps) break;
-      body(sQ2, sO2, sL2, sD2, sQ1, sO1, sL1, sD1);
+      body(sQ2, sO2, sD2, sQ0, sO0, sL0, sQ1, sO1, sL1, sD1);
     }
   };
   if (role_dk) run(std::true_type{});
