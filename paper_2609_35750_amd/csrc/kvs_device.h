@@ -100,6 +100,41 @@ __device__ __forceinline__ uint2 pack4_bf16(float a, float b, float c, float d) 
 
 __device__ __forceinline__ float wave_xor32(float x) { return __shfl_xor(x, 32); }
 
+// Asynchronous global -> LDS copy (global_load_lds_dword{,x4}): lane l of the
+// wave writes its 4 or 16 bytes at LDS byte address lds + (4 or 16) l.  Issued
+// through inline assembly so that the compiler does not count the copy as an
+// outstanding LDS access: with a compiler-visible LDS DMA in flight it waits for
+// every earlier LDS read (lgkmcnt(0)) before each use of any of them.  Callers
+// order the copies themselves (wait_vm() and a barrier before the tile is read).
+// M0 holds the LDS base during the copy and is restored afterwards.
+__device__ __forceinline__ uint32_t lds_addr(const void* lds) {
+  return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void*)lds);
+}
+// base: wave-uniform global address; off: this lane's byte offset from it.
+__device__ __forceinline__ void dma_b128(const void* base, uint32_t off, uint32_t lds) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %3\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2\n\ts_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(off), "s"(base), "s"(lds)
+      : "memory");
+}
+__device__ __forceinline__ void dma_b32(const void* base, uint32_t off, uint32_t lds) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %3\n\ts_nop 0\n\tglobal_load_lds_dword %1, %2\n\ts_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(off), "s"(base), "s"(lds)
+      : "memory");
+}
+// A wave-uniform pointer held in scalar registers.
+template <typename T>
+__device__ __forceinline__ const T* uniform_ptr(const T* p) {
+  const uint64_t u = (uint64_t)(uintptr_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)u), hi = __builtin_amdgcn_readfirstlane((uint32_t)(u >> 32));
+  return (const T*)(uintptr_t)(((uint64_t)hi << 32) | lo);
+}
+
 // LDS tile of rows x D bf16.  Rows are padded (D = 128: 144 elements, D = 64:
 // 72) and, for D = 128, the lowest bit of the 16-byte chunk index is flipped
 // in rows 8..15 of every 16.  Two access patterns are then free of bank
@@ -131,7 +166,7 @@ struct Lay {
   }
 };
 
-// Asynchronous global -> LDS copies of an R-row tile (global_load_lds_dwordx4:
+// Asynchronous global -> LDS copies of an R-row tile (dma_b128:
 // lane l of a wave writes 16 bytes at the wave's LDS base + 16 l, so the 64
 // lanes of one instruction fill 64 consecutive 16-byte slots of the padded
 // tile; padding slots are skipped).  Waves take turns issuing the 64-slot
@@ -161,14 +196,16 @@ struct RowStager {
   }
   // number of copy instructions one call of issue() makes for this wave
   __device__ static __forceinline__ int count(int wave, int nw) { return wave < NI ? (NI - 1 - wave) / nw + 1 : 0; }
+  // row0 <= rmax; rows row0 .. row0 + R - 1 of g (clamped) span less than 4 GiB.
   __device__ __forceinline__ void issue(uint16_t* lds, const uint16_t* __restrict__ g, long long row_stride, int row0,
                                         int rmax, int wave, int nw) const {
+    const uint16_t* base = uniform_ptr(g + (long long)row0 * row_stride);
 #pragma unroll
     for (int i = 0; i < MAXI; ++i) {
       const int n = wave + i * nw;
       if (n < NI) {
-        const int gr = min(row0 + row[i], rmax);
-        __builtin_amdgcn_global_load_lds(g + gr * row_stride + col[i], (lds_void*)(lds + n * kWave * 8), 16, 0, 0);
+        const int dr = min(row0 + row[i], rmax) - row0;
+        dma_b128(base, (uint32_t)(dr * row_stride + col[i]) * 2u, lds_addr(lds + n * kWave * 8));
       }
     }
   }
@@ -176,8 +213,8 @@ struct RowStager {
 
 // 64 consecutive 4-byte values (clamped at index imax) into LDS, by one wave.
 __device__ __forceinline__ void stage_words(void* lds, const void* __restrict__ g, int i0, int imax, int lane) {
-  const int i = min(i0 + lane, imax);
-  __builtin_amdgcn_global_load_lds((const char*)g + 4ll * i, (lds_void*)lds, 4, 0, 0);
+  const char* base = uniform_ptr((const char*)g + 4ll * i0);
+  dma_b32(base, 4u * (uint32_t)(min(i0 + lane, imax) - i0), lds_addr(lds));
 }
 
 // Wait for this wave's outstanding global loads (including LDS-direct ones).

@@ -231,7 +231,7 @@ __device__ __forceinline__ bool row_tile(const RowArgs& a, RowTile& t) {
   t.i0 = qt * BMt;
   t.i1 = t.i0 + BMt;
   if (t.i0 >= t.tr.L) return false;
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   t.hh = wave % a.HG;
   t.h = t.g * a.G + hgrp * a.HG + t.hh;
   t.i0w = t.i0 + 32 * (wave / a.HG);
@@ -270,7 +270,7 @@ __global__ void __launch_bounds__(512) fwd_kernel(RowArgs a) {
 
   RowTile rt;
   if (!row_tile(a, rt)) return;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = blockDim.x >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6), nw = blockDim.x >> 6;
   const int half = lane >> 5, col = lane & 31;
   const Trace tr = rt.tr;
   const int i = rt.i0w + col;
@@ -431,7 +431,7 @@ __global__ void __launch_bounds__(512) dq_kernel(RowArgs a) {
 
   RowTile rt;
   if (!row_tile(a, rt)) return;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = blockDim.x >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6), nw = blockDim.x >> 6;
   const int half = lane >> 5, col = lane & 31;
   const Trace tr = rt.tr;
   const int i = rt.i0w + col;
@@ -568,7 +568,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
   const int j0 = kt * kColKeys;
   if (j0 >= tr.L) return;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const bool role_dk = wave >= 4;
   const int kw = wave & 3;
   const int half = lane >> 5, col = lane & 31;
@@ -682,21 +682,141 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
     sb[1] = pack8(x, 8);
   };
 
+  // Both 32-row blocks FULL (the common case), written as one straight-line
+  // sequence whose order is pinned with scheduling fences: all LDS operands of
+  // the score products are requested before the first product, and the
+  // transposed operands of each accumulation are requested while the
+  // exponentials of that block are computed, so LDS latency overlaps work.
+  auto dv_full = [&](int step, const uint16_t* cQ, const uint16_t* cO, const float* cL) __attribute__((always_inline)) {
+    bf16x8 qa[2][KS];
+    float4 lv[2][4];
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk) {
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) qa[blk][ks] = lds_read_b128(cQ + rl + 32 * blk * PITCH + 16 * ks);
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) lv[blk][q4] = *reinterpret_cast<const float4*>(cL + 32 * blk + 8 * q4 + 4 * half);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    f32x16 x[2];
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk) {
+      x[blk] = f32x16{};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) x[blk] = mfma32(qa[blk][ks], kvreg[ks], x[blk]);
+    }
+    bf16x8 tA[2][DB], tB[2][DB];
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int d = 0; d < DB; ++d) tA[t][d] = tr_operand<D>(cO, 16 * t, 32 * d, tl, th);
+    __builtin_amdgcn_sched_barrier(0);
+    bf16x8 pb[2][2];
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk) {
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const float lq[4] = {lv[blk][q4].x, lv[blk][q4].y, lv[blk][q4].z, lv[blk][q4].w};
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+          x[blk][4 * q4 + t] = __builtin_amdgcn_exp2f(__builtin_fmaf(x[blk][4 * q4 + t], a.scale_log2, -lq[t]));
+      }
+      pb[blk][0] = pack8(x[blk], 0);
+      pb[blk][1] = pack8(x[blk], 8);
+      f16x8 h0, h1;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        h0[e] = (_Float16)x[blk][e];
+        h1[e] = (_Float16)x[blk][8 + e];
+      }
+      *xslot(step, blk, 0) = h0;
+      *xslot(step, blk, 1) = h1;
+      if (blk == 0) {
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+          for (int d = 0; d < DB; ++d) tB[t][d] = tr_operand<D>(cO, 32 + 16 * t, 32 * d, tl, th);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+          for (int d = 0; d < DB; ++d) acc[d] = mfma32(tA[t][d], pb[0][t], acc[d]);
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int d = 0; d < DB; ++d) acc[d] = mfma32(tB[t][d], pb[1][t], acc[d]);
+  };
+  auto dk_full = [&](int step, const uint16_t* cQ, const uint16_t* cO, const float* cD) __attribute__((always_inline)) {
+    bf16x8 oa[2][KS];
+    f32x16 dp[2];
+    f16x8 pr[2][2];
+    float4 dv4[2][4];
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) oa[blk][ks] = lds_read_b128(cO + rl + 32 * blk * PITCH + 16 * ks);
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk) {
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) dv4[blk][q4] = *reinterpret_cast<const float4*>(cD + 32 * blk + 8 * q4 + 4 * half);
+      pr[blk][0] = *xslot(step, blk, 0);
+      pr[blk][1] = *xslot(step, blk, 1);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk) {
+      dp[blk] = f32x16{};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) dp[blk] = mfma32(oa[blk][ks], kvreg[ks], dp[blk]);
+    }
+    bf16x8 tA[2][DB], tB[2][DB];
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int d = 0; d < DB; ++d) tA[t][d] = tr_operand<D>(cQ, 16 * t, 32 * d, tl, th);
+    __builtin_amdgcn_sched_barrier(0);
+    bf16x8 sb[2][2];
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk) {
+      f32x16 x;
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const float dq[4] = {dv4[blk][q4].x, dv4[blk][q4].y, dv4[blk][q4].z, dv4[blk][q4].w};
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const int r = 4 * q4 + t;
+          x[r] = (float)pr[blk][r >> 3][r & 7] * (dp[blk][r] - dq[t]);
+        }
+      }
+      sb[blk][0] = pack8(x, 0);
+      sb[blk][1] = pack8(x, 8);
+      if (blk == 0) {
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+          for (int d = 0; d < DB; ++d) tB[t][d] = tr_operand<D>(cQ, 32 + 16 * t, 32 * d, tl, th);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+          for (int d = 0; d < DB; ++d) acc[d] = mfma32(tA[t][d], sb[0][t], acc[d]);
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int d = 0; d < DB; ++d) acc[d] = mfma32(tB[t][d], sb[1][t], acc[d]);
+  };
   auto dv_step = [&](int step, const uint16_t* cQ, const uint16_t* cO, const float* cL) __attribute__((always_inline)) {
     const int i0 = (qs_lo + step / a.G) * kQStep;
     const int c0 = tile_class(i0, i0 + 32, jw0, jw0 + 32, tr.L, emin_w, emax_w);
     const int c1 = tile_class(i0 + 32, i0 + 64, jw0, jw0 + 32, tr.L, emin_w, emax_w);
     if (c0 == kFull && c1 == kFull) {
-      bf16x8 p0[2], p1[2];
-      f16x8 h0[2], h1[2];
-      dv_block_s(cQ, cL, 0, i0, false, p0, h0);
-      dv_block_s(cQ, cL, 32, i0 + 32, false, p1, h1);
-      *xslot(step, 0, 0) = h0[0];
-      *xslot(step, 0, 1) = h0[1];
-      *xslot(step, 1, 0) = h1[0];
-      *xslot(step, 1, 1) = h1[1];
-      block_acc(cO, 0, p0);
-      block_acc(cO, 32, p1);
+      dv_full(step, cQ, cO, cL);
     } else {
       if (c0 != kEmpty) {
         bf16x8 p0[2];
@@ -721,11 +841,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
     const int c0 = tile_class(i0, i0 + 32, jw0, jw0 + 32, tr.L, emin_w, emax_w);
     const int c1 = tile_class(i0 + 32, i0 + 64, jw0, jw0 + 32, tr.L, emin_w, emax_w);
     if (c0 != kEmpty && c1 != kEmpty) {
-      bf16x8 s0[2], s1[2];
-      dk_block_s(cO, cD, 0, xslot(step, 0, 0), xslot(step, 0, 1), s0);
-      dk_block_s(cO, cD, 32, xslot(step, 1, 0), xslot(step, 1, 1), s1);
-      block_acc(cQ, 0, s0);
-      block_acc(cQ, 32, s1);
+      dk_full(step, cQ, cO, cD);
     } else {
       if (c0 != kEmpty) {
         bf16x8 s0[2];
