@@ -64,8 +64,8 @@ void head_grouping(kvs::Problem& p) {
 }
 
 size_t fwd_ws(int B, long long ntok) { return kvs::ws_kstats_bytes(B, (int)ntok); }
-size_t bwd_ws(int B, long long ntok, int Hq) {
-  return kvs::ws_kstats_bytes(B, (int)ntok) + kvs::ws_delta_bytes(Hq, (int)ntok);
+size_t bwd_ws(int B, int T, long long ntok, int Hq, int Hkv, int D) {
+  return kvs::ws_kstats_bytes(B, (int)ntok) + kvs::ws_delta_bytes(Hq, (int)ntok) + kvs::ws_split_bytes(B, T, Hkv, D);
 }
 
 kvs_status_t check_ws(void* ws, size_t have, size_t need) {
@@ -100,7 +100,8 @@ kvs_status_t run_bwd(kvs::Problem& p) {
   if (e != hipSuccess) return hip_fail(e, "key-tile statistics launch");
   e = kvs::launch_bwd_pre(p, delta);
   if (e != hipSuccess) return hip_fail(e, "backward preprocess launch");
-  e = kvs::launch_bwd_dkdv(p, delta);
+  void* split_ws = (char*)delta + kvs::ws_delta_bytes(p.Hq, p.ntok);
+  e = kvs::launch_bwd_dkdv(p, kstats, delta, split_ws);
   if (e != hipSuccess) return hip_fail(e, "dK/dV launch");
   e = kvs::launch_bwd_dq(p, kstats, delta);
   if (e != hipSuccess) return hip_fail(e, "dQ launch");
@@ -165,9 +166,8 @@ size_t kvs_evict_attn_fwd_workspace(int B, int T, int Hq, int Hkv, int D) {
 }
 
 size_t kvs_evict_attn_bwd_workspace(int B, int T, int Hq, int Hkv, int D) {
-  if (B < 1 || T < 1 || Hq < 1) return 0;
-  (void)Hkv; (void)D;
-  return bwd_ws(B, (long long)B * T, Hq);
+  if (B < 1 || T < 1 || Hq < 1 || Hkv < 1) return 0;
+  return bwd_ws(B, T, (long long)B * T, Hq, Hkv, D);
 }
 
 size_t kvs_evict_attn_varlen_fwd_workspace(int B, int Ntot, int max_seqlen, int Hq, int Hkv, int D) {
@@ -177,9 +177,8 @@ size_t kvs_evict_attn_varlen_fwd_workspace(int B, int Ntot, int max_seqlen, int 
 }
 
 size_t kvs_evict_attn_varlen_bwd_workspace(int B, int Ntot, int max_seqlen, int Hq, int Hkv, int D) {
-  if (B < 1 || Ntot < 0 || Hq < 1) return 0;
-  (void)max_seqlen; (void)Hkv; (void)D;
-  return bwd_ws(B, Ntot, Hq);
+  if (B < 1 || Ntot < 0 || Hq < 1 || Hkv < 1 || max_seqlen < 1) return 0;
+  return bwd_ws(B, max_seqlen, Ntot, Hq, Hkv, D);
 }
 
 static kvs_status_t fwd_common(const void* Q, const void* K, const void* V, const int32_t* evict_at,
@@ -223,7 +222,7 @@ static kvs_status_t bwd_common(const void* dO, const void* Q, const void* K, con
   REQUIRE_PTR(dV, "dV");
   if (!evict_at) return fail(KVS_ERR_NULL, "evict_at is NULL");
   if (!(scale > 0.f) || scale != scale) return fail(KVS_ERR_SHAPE, "softmax_scale must be positive and finite");
-  st = check_ws(ws, ws_bytes, bwd_ws(B, ntok, Hq));
+  st = check_ws(ws, ws_bytes, bwd_ws(B, T, ntok, Hq, Hkv, D));
   if (st != KVS_OK) return st;
   if (ntok == 0) return KVS_OK;
   kvs::Problem p{};

@@ -23,6 +23,7 @@
 #include "kvs_device.h"
 #include "kvs_launch.h"
 
+#include <algorithm>
 #include <climits>
 #include <type_traits>
 
@@ -59,11 +60,19 @@ struct ColArgs {
   const int* cu;
   uint16_t* dk;
   uint16_t* dv;
+  const int* plan;      // [B * nkt][2]: chunks of the key block (1 = not split), first slot
+  const int2* items;    // [B * nkt + capE]: (key block, chunk) work items, longest first; (-1, 0) unused
+  float* part;          // [capE * Hkv][2][kColKeys][D] fp32 partial dV, dK of split blocks
   int B, T, Hq, Hkv, G, nkt, ntok;
+  int capE;             // slots per KV head (0: no splitting)
   int varlen;
   float scale_log2;
   float scale;
 };
+
+// Row-step chunk of a split key block: 64 row-steps of 64 query rows; blocks
+// whose span exceeds two chunks are split (see split_plan_kernel).
+constexpr int kSplitRowSteps = 64;
 
 // LSE / Delta layout: fixed [B][Hq][T], varlen [Hq][ntok].
 __device__ __forceinline__ long long lse_index(int varlen, int ntok, int Hq, int T, int b, int h, int tok0, int i) {
@@ -558,12 +567,13 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
   __shared__ __attribute__((aligned(1024))) f16x8 sP[2 * 4 * 2 * 2 * kWave];
   __shared__ int sEmax[4];
 
-  int wg = blockIdx.x;
-  const int g = wg % a.Hkv;
-  wg /= a.Hkv;
-  const int b = wg % a.B;
-  wg /= a.B;
-  const int kt = wg;
+  // Work item of this workgroup (longest first, see split_plan_kernel): a
+  // whole key block, or one row chunk of a split block; one KV head each.
+  const int g = blockIdx.x % a.Hkv;
+  const int2 item = a.items[blockIdx.x / a.Hkv];
+  if (item.x < 0) return;   // unused list entry
+  const int b = item.x / a.nkt, kt = item.x % a.nkt, chunk = item.y;
+  const int nchunk = a.plan[2 * item.x], slot0 = a.plan[2 * item.x + 1];
   const Trace tr = trace_of(a.cu, b, a.T);
   const int j0 = kt * kColKeys;
   if (j0 >= tr.L) return;
@@ -598,9 +608,13 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
   }
   __syncthreads();
   const int emax_wg = max(max(sEmax[0], sEmax[1]), max(sEmax[2], sEmax[3]));
-  const int qs_lo = j0 / kQStep;
-  const int qs_hi = (emax_wg + kQStep - 1) / kQStep;
-  const int steps = (qs_hi - qs_lo) * a.G;
+  int qs_lo = j0 / kQStep;
+  int qs_hi = (emax_wg + kQStep - 1) / kQStep;
+  if (nchunk > 1) {
+    qs_lo += chunk * kSplitRowSteps;
+    qs_hi = min(qs_hi, qs_lo + kSplitRowSteps);
+  }
+  const int steps = max(qs_hi - qs_lo, 0) * a.G;
 
   f32x16 acc[DB];   // dV^T (dV waves) or dK^T (dK waves): rows d, column = this lane's key
 #pragma unroll
@@ -887,7 +901,17 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
   if (role_dk) run(std::true_type{});
   else run(std::false_type{});
 
-  if (key_ok) {
+  if (nchunk > 1) {
+    // fp32 partial sums of this chunk: [slot][dV, dK][key in block][d]
+    float* dst = a.part + (((size_t)(slot0 + chunk) * a.Hkv + g) * 2 + (role_dk ? 1 : 0)) * kColKeys * D +
+                 (size_t)(32 * kw + col) * D;
+#pragma unroll
+    for (int d = 0; d < DB; ++d)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4)
+        *reinterpret_cast<float4*>(dst + 32 * d + 8 * q4 + 4 * half) =
+            make_float4(acc[d][4 * q4], acc[d][4 * q4 + 1], acc[d][4 * q4 + 2], acc[d][4 * q4 + 3]);
+  } else if (key_ok) {
     const size_t koff = ((size_t)(tr.tok0 + j) * a.Hkv + g) * D;
     uint16_t* dst = role_dk ? a.dk + koff : a.dv + koff;
     const float sc = role_dk ? a.scale : 1.f;
@@ -900,6 +924,130 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
   }
 }
 
+// ---------------------------------------------------------------- work plan of the column kernel
+// A key block whose keys stay visible for many query rows (the prompt,
+// long-lived summaries) would be one long workgroup and set the kernel's
+// critical path.  Blocks spanning more than 2 * kSplitRowSteps row-steps are
+// cut into chunks of kSplitRowSteps row-steps; every chunk gets a slot of fp32
+// partial sums, and the chunks are added in slot order afterwards
+// (deterministic).  Slots are granted in key-block order while capE lasts;
+// later blocks stay whole.  All work items (whole blocks and chunks) are then
+// listed longest first (counting sort on the row-step count), so the longest
+// items start first.  One workgroup of 1024 threads; block spans come from the
+// 64-key tile statistics.
+__global__ void __launch_bounds__(1024) split_plan_kernel(const int2* __restrict__ kstats, const int* __restrict__ cu,
+                                                          int B, int T, int nkt, int capE, int* __restrict__ plan,
+                                                          int2* __restrict__ items) {
+  constexpr int NBK = 2048;   // sort buckets: row-step counts 0 .. 2047 (longer ones share the last bucket)
+  __shared__ int scan[1024];
+  __shared__ int bucket[NBK];
+  const int tid = threadIdx.x;
+  const int nblocks = B * nkt, nitems = nblocks + capE;
+  for (int i = tid; i < NBK; i += 1024) bucket[i] = 0;
+  for (int e = tid; e < nitems; e += 1024) items[e] = make_int2(-1, 0);
+  const int per = (nblocks + 1023) / 1024;
+  const int b0 = min(tid * per, nblocks), b1 = min(b0 + per, nblocks);
+  auto span_of = [&](int blk) {   // query row-steps [j0/64, ceil(emax/64)) of the block; 0 past the trace
+    const int b = blk / nkt, kt = blk % nkt;
+    const Trace tr = trace_of(cu, b, T);
+    const int j0 = kt * kColKeys;
+    if (j0 >= tr.L) return 0;
+    const int t0 = j0 / kKeyTile, nt = (tr.L + kKeyTile - 1) / kKeyTile;
+    int emax = kstats[kstat_index(b, tr.tok0, t0, kKeyTile)].y;
+    if (t0 + 1 < nt) emax = max(emax, kstats[kstat_index(b, tr.tok0, t0 + 1, kKeyTile)].y);
+    return (emax + kQStep - 1) / kQStep - j0 / kQStep;
+  };
+  auto chunks_of = [](int span) {
+    return span > 2 * kSplitRowSteps ? (span + kSplitRowSteps - 1) / kSplitRowSteps : 0;
+  };
+  auto key_of = [](int rows) { return min(rows, NBK - 1); };
+  int tot = 0;
+  for (int blk = b0; blk < b1; ++blk) tot += chunks_of(span_of(blk));
+  scan[tid] = tot;
+  __syncthreads();
+  for (int off = 1; off < 1024; off <<= 1) {
+    const int v = tid >= off ? scan[tid - off] : 0;
+    __syncthreads();
+    scan[tid] += v;
+    __syncthreads();
+  }
+  int run = scan[tid] - tot;   // exclusive prefix of requested slots
+  for (int blk = b0; blk < b1; ++blk) {
+    const int span = span_of(blk), w = chunks_of(span);
+    const bool grant = w > 0 && run + w <= capE;
+    plan[2 * blk] = grant ? w : 1;
+    plan[2 * blk + 1] = grant ? run : 0;
+    run += w;
+    if (span == 0) continue;
+    if (grant)
+      for (int c = 0; c < w; ++c) atomicAdd(&bucket[key_of(min(kSplitRowSteps, span - c * kSplitRowSteps))], 1);
+    else
+      atomicAdd(&bucket[key_of(span)], 1);
+  }
+  __syncthreads();
+  // bucket start positions, longest first: thread t owns buckets NBK-1-2t and NBK-2-2t
+  const int khi = NBK - 1 - 2 * tid, klo = khi - 1;
+  const int chi = bucket[khi], clo = bucket[klo];
+  scan[tid] = chi + clo;
+  __syncthreads();
+  for (int off = 1; off < 1024; off <<= 1) {
+    const int v = tid >= off ? scan[tid - off] : 0;
+    __syncthreads();
+    scan[tid] += v;
+    __syncthreads();
+  }
+  const int excl = scan[tid] - chi - clo;
+  bucket[khi] = excl;
+  bucket[klo] = excl + chi;
+  __syncthreads();
+  for (int blk = b0; blk < b1; ++blk) {
+    const int span = span_of(blk);
+    if (span == 0) continue;
+    const int nc = plan[2 * blk];
+    if (nc > 1) {
+      for (int c = 0; c < nc; ++c)
+        items[atomicAdd(&bucket[key_of(min(kSplitRowSteps, span - c * kSplitRowSteps))], 1)] = make_int2(blk, c);
+    } else {
+      items[atomicAdd(&bucket[key_of(span)], 1)] = make_int2(blk, 0);
+    }
+  }
+}
+
+// Sum of the chunk partials of split key blocks, in chunk order; dK scaled.
+// One workgroup per (key block, KV head); blocks that were not split exit.
+template <int D>
+__global__ void __launch_bounds__(256) split_reduce_kernel(const int* __restrict__ plan, const float* __restrict__ part,
+                                                           const int* __restrict__ cu, uint16_t* __restrict__ dk,
+                                                           uint16_t* __restrict__ dv, int B, int T, int nkt, int Hkv,
+                                                           float scale) {
+  const int g = blockIdx.x % Hkv, blk = blockIdx.x / Hkv;
+  const int nc = plan[2 * blk], s0 = plan[2 * blk + 1];
+  if (nc <= 1) return;
+  const int b = blk / nkt, kt = blk % nkt;
+  const Trace tr = trace_of(cu, b, T);
+  constexpr int PER = kColKeys * D / 256;   // elements per thread (multiple of 4)
+  for (int which = 0; which < 2; ++which) {
+    for (int q = 0; q < PER / 4; ++q) {
+      const int e = (q * 256 + threadIdx.x) * 4;   // element of [key][d]
+      const int key = e / D, d = e % D;
+      float4 sum = make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int c = 0; c < nc; ++c) {
+        const float4 v = *reinterpret_cast<const float4*>(part + (((size_t)(s0 + c) * Hkv + g) * 2 + which) * kColKeys * D + e);
+        sum.x += v.x;
+        sum.y += v.y;
+        sum.z += v.z;
+        sum.w += v.w;
+      }
+      const int j = kt * kColKeys + key;
+      if (j < tr.L) {
+        const float sc = which ? scale : 1.f;
+        uint16_t* dst = (which ? dk : dv) + ((size_t)(tr.tok0 + j) * Hkv + g) * D + d;
+        *reinterpret_cast<uint2*>(dst) = pack4_bf16(sum.x * sc, sum.y * sc, sum.z * sc, sum.w * sc);
+      }
+    }
+  }
+}
+
 // Explicit instantiations: every kernel the launchers use is emitted, with its host stub.
 template __global__ void fwd_kernel<64>(RowArgs);
 template __global__ void fwd_kernel<128>(RowArgs);
@@ -907,6 +1055,10 @@ template __global__ void dq_kernel<64>(RowArgs);
 template __global__ void dq_kernel<128>(RowArgs);
 template __global__ void dkdv_kernel<64>(ColArgs);
 template __global__ void dkdv_kernel<128>(ColArgs);
+template __global__ void split_reduce_kernel<64>(const int*, const float*, const int*, uint16_t*, uint16_t*, int, int,
+                                                 int, int, float);
+template __global__ void split_reduce_kernel<128>(const int*, const float*, const int*, uint16_t*, uint16_t*, int, int,
+                                                  int, int, float);
 
 // ---------------------------------------------------------------- launchers
 size_t ws_kstats_bytes(int B, int ntok) {
@@ -916,6 +1068,27 @@ size_t ws_kstats_bytes(int B, int ntok) {
 
 // Delta followed by LSE * log2(e), each [Hq][ntok] (or [B][Hq][T]) fp32.
 size_t ws_delta_bytes(int Hq, int ntok) { return 2 * (((size_t)Hq * ntok * sizeof(float) + 255) & ~(size_t)255); }
+
+static size_t round256(size_t n) { return (n + 255) & ~(size_t)255; }
+
+// Work plan of the column kernel: plan [B * nkt][2] int, work items
+// [B * nkt + capE] int2, partial sums [capE * Hkv][2][kColKeys][D] fp32.
+// capE: chunk slots per KV head, at most 2048 slots over all KV heads, none
+// when no block can span more than two chunks.
+int split_cap(int B, int T, int Hkv) {
+  const int max_span = (T + kQStep - 1) / kQStep;
+  if (max_span <= 2 * kSplitRowSteps) return 0;
+  const long long nkt = (T + kColKeys - 1) / kColKeys;
+  const long long per_block = (max_span + kSplitRowSteps - 1) / kSplitRowSteps;
+  const long long cap = std::min<long long>(2048 / Hkv, (long long)B * nkt * per_block);
+  return (int)std::max<long long>(cap, 0);
+}
+size_t ws_split_bytes(int B, int T, int Hkv, int D) {
+  const int capE = split_cap(B, T, Hkv);
+  const long long nkt = (T + kColKeys - 1) / kColKeys;
+  return round256((size_t)B * nkt * 2 * sizeof(int)) + round256(((size_t)B * nkt + capE) * sizeof(int2)) +
+         round256((size_t)capE * Hkv * 2 * kColKeys * D * sizeof(float));
+}
 static size_t half_delta_bytes(int Hq, int ntok) { return ws_delta_bytes(Hq, ntok) / 2; }
 
 static RowArgs row_args(const Problem& p, const int2* kstats) {
@@ -981,7 +1154,7 @@ hipError_t launch_bwd_pre(const Problem& p, float* delta) {
   return hipGetLastError();
 }
 
-hipError_t launch_bwd_dkdv(const Problem& p, const float* delta) {
+hipError_t launch_bwd_dkdv(const Problem& p, const int2* kstats, const float* delta, void* split_ws) {
   ColArgs a{};
   a.q = (const uint16_t*)p.q;
   a.k = (const uint16_t*)p.k;
@@ -1003,11 +1176,35 @@ hipError_t launch_bwd_dkdv(const Problem& p, const float* delta) {
   a.varlen = p.cu != nullptr;
   a.scale = p.scale;
   a.scale_log2 = p.scale * 1.4426950408889634f;
-  const long long nblk = (long long)a.nkt * p.B * p.Hkv;
+  a.capE = split_cap(p.B, p.T, p.Hkv);
+  {
+    char* w = (char*)split_ws;
+    int* plan = (int*)w;
+    w += round256((size_t)p.B * a.nkt * 2 * sizeof(int));
+    int2* items = (int2*)w;
+    w += round256(((size_t)p.B * a.nkt + a.capE) * sizeof(int2));
+    a.plan = plan;
+    a.items = items;
+    a.part = (float*)w;
+    hipLaunchKernelGGL(split_plan_kernel, dim3(1), dim3(1024), 0, p.stream, kstats, p.cu, p.B, p.T, a.nkt, a.capE,
+                       plan, items);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  const long long nblk = ((long long)a.nkt * p.B + a.capE) * p.Hkv;
   prof_begin("bwd_dkdv", p.stream);
   if (p.D == 128) hipLaunchKernelGGL(dkdv_kernel<128>, dim3((unsigned)nblk), dim3(512), 0, p.stream, a);
   else hipLaunchKernelGGL(dkdv_kernel<64>, dim3((unsigned)nblk), dim3(512), 0, p.stream, a);
   prof_end(p.stream);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.capE == 0) return e;
+  const dim3 rgrid((unsigned)((long long)p.B * a.nkt * p.Hkv));
+  if (p.D == 128)
+    hipLaunchKernelGGL(split_reduce_kernel<128>, rgrid, dim3(256), 0, p.stream, a.plan, a.part, p.cu,
+                       (uint16_t*)p.dk, (uint16_t*)p.dv, p.B, p.T, a.nkt, p.Hkv, p.scale);
+  else
+    hipLaunchKernelGGL(split_reduce_kernel<64>, rgrid, dim3(256), 0, p.stream, a.plan, a.part, p.cu,
+                       (uint16_t*)p.dk, (uint16_t*)p.dv, p.B, p.T, a.nkt, p.Hkv, p.scale);
   return hipGetLastError();
 }
 

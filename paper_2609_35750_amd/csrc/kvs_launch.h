@@ -35,12 +35,13 @@ struct Problem {
 // Workspace pieces (byte offsets from the workspace start).
 size_t ws_kstats_bytes(int B, int ntok);
 size_t ws_delta_bytes(int Hq, int ntok);
+size_t ws_split_bytes(int B, int T, int Hkv, int D);
 
 // Launchers.  Each returns the hipError_t of its launch(es).
 hipError_t launch_kstats(const Problem& p, int BN, int2* kstats);
 hipError_t launch_fwd(const Problem& p, const int2* kstats);
 hipError_t launch_bwd_pre(const Problem& p, float* delta);
-hipError_t launch_bwd_dkdv(const Problem& p, const float* delta);
+hipError_t launch_bwd_dkdv(const Problem& p, const int2* kstats, const float* delta, void* split_ws);
 hipError_t launch_bwd_dq(const Problem& p, const int2* kstats, const float* delta);
 hipError_t launch_classify(const int32_t* evict, const int32_t* cu, int B, int T, int BM, int BN,
                            uint8_t* out, hipStream_t stream);

@@ -82,6 +82,27 @@ def test_varlen_ragged(kvs):
     _parity(kvs, wl, wl.evict_at(), cu=wl.cu_seqlens())
 
 
+# Traces past 8192 rows have key blocks (the prompt) visible to more than two
+# 4096-row chunks: the dK/dV work is then split into row chunks whose fp32
+# partial sums are added afterwards.  Element-by-element parity and bitwise
+# reproducibility of that path, fixed-length and packed.
+@pytest.mark.parametrize("L,Hq,Hkv,D", [(8704, 2, 1, 64), (8385, 4, 2, 128)])
+def test_long_key_spans_split(kvs, L, Hq, Hkv, D):
+    wl = inputs.custom_workload(f"split_L{L}", Hq, Hkv, D, [L], 256, 2048, 128, "keep_all", seed=L + 5)
+    _parity(kvs, wl, wl.evict_at())
+    t = inputs.make_tensors(wl)
+    a = gpu_fwd_bwd(kvs, t["q"], t["k"], t["v"], t["do"], wl.evict_at(), wl.softmax_scale)
+    b = gpu_fwd_bwd(kvs, t["q"], t["k"], t["v"], t["do"], wl.evict_at(), wl.softmax_scale)
+    for key in ("dk", "dv"):
+        assert torch.equal(a[key], b[key]), key
+
+
+def test_long_key_spans_split_varlen(kvs):
+    wl = inputs.custom_workload("split_varlen", 4, 2, 64, [700, 8500, 129], 300, 1500, 100, "last2", varlen=True,
+                                seed=31)
+    _parity(kvs, wl, wl.evict_at(), cu=wl.cu_seqlens())
+
+
 def test_self_only_closed_form(kvs):
     # every key lives for one query: O_i = v_i, dQ = dK = 0, dV_j = sum over the group of dO_j
     L, Hq, Hkv, D = 200, 4, 2, 128
