@@ -181,10 +181,11 @@ struct RowStager {
   using LY = Lay<D>;
   static constexpr int NI = R * LY::CPRP / kWave;   // 64-slot pieces per tile
   static_assert(R * LY::CPRP % kWave == 0, "tile must fill whole 64-slot pieces");
-  int row[MAXI];   // tile row of this lane's slot, or -1 (no piece)
-  int col[MAXI];   // element column of the slot's first element in the source row
+  int row[MAXI];        // tile row of this lane's slot, or -1 (no piece)
+  int col[MAXI];        // element column of the slot's first element in the source row
+  uint32_t off[MAXI];   // byte offset of the slot's source from the tile's first row (no clamping)
 
-  __device__ __forceinline__ void init(int wave, int nw, int lane) {
+  __device__ __forceinline__ void init(int wave, int nw, int lane, long long row_stride) {
 #pragma unroll
     for (int i = 0; i < MAXI; ++i) {
       const int n = wave + i * nw;
@@ -192,29 +193,39 @@ struct RowStager {
       const int r = q / LY::CPRP, pc = q - r * LY::CPRP;
       row[i] = n < NI ? r : -1;
       col[i] = (n < NI && pc < LY::CPR) ? 8 * (pc ^ LY::flip(r)) : 0;
+      off[i] = n < NI ? (uint32_t)(r * row_stride + col[i]) * 2u : 0u;
     }
   }
   // number of copy instructions one call of issue() makes for this wave
   __device__ static __forceinline__ int count(int wave, int nw) { return wave < NI ? (NI - 1 - wave) / nw + 1 : 0; }
-  // row0 <= rmax; rows row0 .. row0 + R - 1 of g (clamped) span less than 4 GiB.
-  __device__ __forceinline__ void issue(uint16_t* lds, const uint16_t* __restrict__ g, long long row_stride, int row0,
+  // row0 <= rmax; rows row0 .. row0 + R - 1 of g (clamped) span less than 4 GiB; row_stride as given to init().
+  // lds: LDS byte address of the tile (lds_addr).
+  __device__ __forceinline__ void issue(uint32_t lds, const uint16_t* __restrict__ g, long long row_stride, int row0,
                                         int rmax, int wave, int nw) const {
     const uint16_t* base = uniform_ptr(g + (long long)row0 * row_stride);
+    if (row0 + R - 1 <= rmax) {   // whole tile inside: precomputed offsets
 #pragma unroll
-    for (int i = 0; i < MAXI; ++i) {
-      const int n = wave + i * nw;
-      if (n < NI) {
-        const int dr = min(row0 + row[i], rmax) - row0;
-        dma_b128(base, (uint32_t)(dr * row_stride + col[i]) * 2u, lds_addr(lds + n * kWave * 8));
+      for (int i = 0; i < MAXI; ++i) {
+        const int n = wave + i * nw;
+        if (n < NI) dma_b128(base, off[i], lds + n * kWave * 16);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < MAXI; ++i) {
+        const int n = wave + i * nw;
+        if (n < NI) {
+          const int dr = min(row0 + row[i], rmax) - row0;
+          dma_b128(base, (uint32_t)(dr * row_stride + col[i]) * 2u, lds + n * kWave * 16);
+        }
       }
     }
   }
 };
 
 // 64 consecutive 4-byte values (clamped at index imax) into LDS, by one wave.
-__device__ __forceinline__ void stage_words(void* lds, const void* __restrict__ g, int i0, int imax, int lane) {
+__device__ __forceinline__ void stage_words(uint32_t lds, const void* __restrict__ g, int i0, int imax, int lane) {
   const char* base = uniform_ptr((const char*)g + 4ll * i0);
-  dma_b32(base, 4u * (uint32_t)(min(i0 + lane, imax) - i0), lds_addr(lds));
+  dma_b32(base, 4u * (uint32_t)(min(i0 + lane, imax) - i0), lds);
 }
 
 // Wait for this wave's outstanding global loads (including LDS-direct ones).

@@ -257,9 +257,9 @@ __device__ __forceinline__ void stage_kv(const KVStager<D>& st, uint16_t* sK, ui
   const int j0 = kt * kKeyTile;
   const long long base = ((long long)rt.tr.tok0 * a.Hkv + rt.g) * D;
   const long long stride = (long long)a.Hkv * D;
-  st.issue(sK, a.k + base, stride, j0, rt.tr.L - 1, wave, nw);
-  st.issue(sV, a.v + base, stride, j0, rt.tr.L - 1, wave, nw);
-  if (wave == nw - 1) stage_words(sE, a.evict + rt.tr.tok0, j0, rt.tr.L - 1, lane);
+  st.issue(lds_addr(sK), a.k + base, stride, j0, rt.tr.L - 1, wave, nw);
+  st.issue(lds_addr(sV), a.v + base, stride, j0, rt.tr.L - 1, wave, nw);
+  if (wave == nw - 1) stage_words(lds_addr(sE), a.evict + rt.tr.tok0, j0, rt.tr.L - 1, lane);
 }
 
 // ---------------------------------------------------------------- forward
@@ -286,7 +286,7 @@ __global__ void __launch_bounds__(512) fwd_kernel(RowArgs a) {
   const bool row_ok = i < tr.L;
   const int rl = Lay<D>::row_lane(lane), tl = Lay<D>::tr_lo(lane), th = Lay<D>::tr_hi(lane);
   KVStager<D> kvst;
-  kvst.init(wave, nw, lane);
+  kvst.init(wave, nw, lane, (long long)a.Hkv * D);
 
   bf16x8 qreg[KS];
   {
@@ -447,7 +447,7 @@ __global__ void __launch_bounds__(512) dq_kernel(RowArgs a) {
   const bool row_ok = i < tr.L;
   const int rl = Lay<D>::row_lane(lane), tl = Lay<D>::tr_lo(lane), th = Lay<D>::tr_hi(lane);
   KVStager<D> kvst;
-  kvst.init(wave, nw, lane);
+  kvst.init(wave, nw, lane, (long long)a.Hkv * D);
   const int ic = min(i, tr.L - 1);
 
   bf16x8 qreg[KS], oreg[KS];
@@ -596,7 +596,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
   }
   if (!role_dk && lane == 0) sEmax[kw] = emax_w;
   RowStager<D, kQStep, 3> qst;
-  qst.init(wave, 8, lane);
+  qst.init(wave, 8, lane, (long long)a.Hq * D);
 
   // K (dV waves) or V (dK waves) of this lane's key: the B operand of S or dP
   bf16x8 kvreg[KS];
@@ -624,11 +624,11 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
     const int i0 = (qs_lo + step / a.G) * kQStep;
     const int h = g * a.G + step % a.G;
     const long long base = ((long long)tr.tok0 * a.Hq + h) * D;
-    qst.issue(q_, a.q + base, (long long)a.Hq * D, i0, tr.L - 1, wave, 8);
-    qst.issue(o_, a.dout + base, (long long)a.Hq * D, i0, tr.L - 1, wave, 8);
+    qst.issue(lds_addr(q_), a.q + base, (long long)a.Hq * D, i0, tr.L - 1, wave, 8);
+    qst.issue(lds_addr(o_), a.dout + base, (long long)a.Hq * D, i0, tr.L - 1, wave, 8);
     const long long lb = lse_index(a.varlen, a.ntok, a.Hq, a.T, b, h, tr.tok0, 0);
-    if (wave == 6) stage_words(l_, a.lse + lb, i0, tr.L - 1, lane);   // LSE * log2(e)
-    if (wave == 7) stage_words(d_, a.delta + lb, i0, tr.L - 1, lane);
+    if (wave == 6) stage_words(lds_addr(l_), a.lse + lb, i0, tr.L - 1, lane);   // LSE * log2(e)
+    if (wave == 7) stage_words(lds_addr(d_), a.delta + lb, i0, tr.L - 1, lane);
   };
   const int jw0 = j0 + 32 * kw;
   auto xslot = [&](int step, int blk, int t) __attribute__((always_inline)) { return sP + ((((step & 1) * 4 + kw) * 2 + blk) * 2 + t) * kWave + lane; };
