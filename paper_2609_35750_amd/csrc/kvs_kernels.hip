@@ -1014,21 +1014,25 @@ __global__ void __launch_bounds__(1024) split_plan_kernel(const int2* __restrict
 }
 
 // Sum of the chunk partials of split key blocks, in chunk order; dK scaled.
-// One workgroup per (key block, KV head); blocks that were not split exit.
+// kReduceSplit workgroups per (key block, KV head), each summing a slice of
+// the block's keys; blocks that were not split exit.
+constexpr int kReduceSplit = 8;
 template <int D>
 __global__ void __launch_bounds__(256) split_reduce_kernel(const int* __restrict__ plan, const float* __restrict__ part,
                                                            const int* __restrict__ cu, uint16_t* __restrict__ dk,
                                                            uint16_t* __restrict__ dv, int B, int T, int nkt, int Hkv,
                                                            float scale) {
-  const int g = blockIdx.x % Hkv, blk = blockIdx.x / Hkv;
+  const int sub = blockIdx.x % kReduceSplit, wg = blockIdx.x / kReduceSplit;
+  const int g = wg % Hkv, blk = wg / Hkv;
   const int nc = plan[2 * blk], s0 = plan[2 * blk + 1];
   if (nc <= 1) return;
   const int b = blk / nkt, kt = blk % nkt;
   const Trace tr = trace_of(cu, b, T);
-  constexpr int PER = kColKeys * D / 256;   // elements per thread (multiple of 4)
+  constexpr int PER = kColKeys * D / kReduceSplit / 256;   // elements per thread
+  static_assert(PER % 4 == 0 && PER >= 4, "reduce slice must be whole float4s per thread");
   for (int which = 0; which < 2; ++which) {
     for (int q = 0; q < PER / 4; ++q) {
-      const int e = (q * 256 + threadIdx.x) * 4;   // element of [key][d]
+      const int e = sub * (kColKeys * D / kReduceSplit) + (q * 256 + threadIdx.x) * 4;   // element of [key][d]
       const int key = e / D, d = e % D;
       float4 sum = make_float4(0.f, 0.f, 0.f, 0.f);
       for (int c = 0; c < nc; ++c) {
@@ -1198,7 +1202,7 @@ hipError_t launch_bwd_dkdv(const Problem& p, const int2* kstats, const float* de
   prof_end(p.stream);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.capE == 0) return e;
-  const dim3 rgrid((unsigned)((long long)p.B * a.nkt * p.Hkv));
+  const dim3 rgrid((unsigned)((long long)p.B * a.nkt * p.Hkv * kReduceSplit));
   if (p.D == 128)
     hipLaunchKernelGGL(split_reduce_kernel<128>, rgrid, dim3(256), 0, p.stream, a.plan, a.part, p.cu,
                        (uint16_t*)p.dk, (uint16_t*)p.dv, p.B, p.T, a.nkt, p.Hkv, p.scale);
