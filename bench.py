@@ -56,6 +56,71 @@ def load_traffic(kernel, workload):
     return rec.get("bytes_per_launch")
 
 
+def reprefill_batch(wl):
+    """The varlen batch re-prefill compaction would run for the same rollouts:
+    per trace, the fresh causal traces of inputs.reprefill_traces."""
+    from paper_2609_35750_amd import inputs
+
+    lengths, extra_exact, extra_formula = [], 0, 0.0
+    for L in wl.lengths:
+        lengths += [len(t) for t in inputs.reprefill_traces(L, wl.p, wl.w, wl.s, wl.strategy)]
+        ex = inputs.reprefill_extra_tokens(L, wl.p, wl.w, wl.s, wl.strategy)
+        extra_exact += ex["extra_exact"]
+        extra_formula += ex["extra_formula"]
+    return lengths, extra_exact, extra_formula
+
+
+def time_steps(step, warmup, steps):
+    import torch
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) * 1e3 / steps
+
+
+def reprefill_compare(wl, kvs, warmup, steps, kvs_ms):
+    """Kernel-level analogue of the paper's re-prefill comparison (Section 2,
+    "Prefill-compaction"): the same library, forward + backward, over the
+    causal traces re-prefill compaction would run instead of one masked trace."""
+    import torch
+
+    from paper_2609_35750_amd import inputs
+
+    lengths, extra_exact, extra_formula = reprefill_batch(wl)
+    n = int(sum(lengths))
+    dev = torch.device("cuda:0")
+    qs = 1.0 / math.sqrt(wl.D) if wl.q_prescaled else 1.0
+    q = inputs.randn_bf16((n, wl.Hq, wl.D), wl.seed * 16 + 9, qs).to(dev)
+    k = inputs.randn_bf16((n, wl.Hkv, wl.D), wl.seed * 16 + 10).to(dev)
+    v = inputs.randn_bf16((n, wl.Hkv, wl.D), wl.seed * 16 + 11).to(dev)
+    do = inputs.randn_bf16((n, wl.Hq, wl.D), wl.seed * 16 + 12).to(dev)
+    ev = torch.from_numpy(np.concatenate([np.full(L, L, dtype=np.int32) for L in lengths])).to(dev)   # never evicted
+    cu_np = np.concatenate([[0], np.cumsum(lengths)]).astype(np.int32)
+    cu = torch.from_numpy(cu_np).to(dev)
+    T = int(max(lengths))
+    kvs.kvs_evict_attn_fwd(q, k, v, ev, wl.softmax_scale, cu, T)   # validates cu_seqlens once
+    o = torch.empty_like(q)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    lse = None
+
+    def step():
+        nonlocal lse
+        _, lse = kvs.kvs_evict_attn_fwd(q, k, v, ev, wl.softmax_scale, cu, T, out=o, lse=lse, check_cu=False)
+        kvs.kvs_evict_attn_bwd(do, q, k, v, o, lse, ev, wl.softmax_scale, cu, T, dq=dq, dk=dk, dv=dv, check_cu=False)
+
+    ms = time_steps(step, warmup, steps)
+    pairs = int(sum(L * (L + 1) // 2 for L in lengths))
+    return {"traces": len(lengths), "tokens": n, "tokens_kv_streams": wl.ntok,
+            "extra_tokens_exact": int(extra_exact), "extra_tokens_formula_Nr_over_B_minus_r": round(extra_formula, 1),
+            "visible_pairs_per_head": pairs, "ms_per_step": ms, "kv_streams_ms_per_step": kvs_ms,
+            "time_ratio_reprefill_over_kv_streams": ms / kvs_ms}
+
+
 def cpu_baseline(wl, tensors, evict_at, heads=2):
     """The fp64 checker as it stands, timed on q-heads [0, heads) of KV head 0."""
     from oracle import attention as orc
@@ -88,6 +153,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="trace16k_gqa4")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU checker timing")
+    ap.add_argument("--no-reprefill", action="store_true", help="skip the re-prefill comparison")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (see DESIGN.md for how it would "
@@ -177,6 +243,9 @@ def main():
         "kernels_ms": {k_: round(v_["avg_ms"], 4) for k_, v_ in per_kernel.items()},
         "roofline": roofline,
     }
+    out["value_strict_12D"] = 12 * wl.D * wl.Hq * vis / (ms_per_step * 1e-3) / 1e12   # no recompute counted
+    if not args.no_reprefill:
+        out["reprefill"] = reprefill_compare(wl, kvs, args.warmup, args.steps, ms_per_step)
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(wl, tensors, e)
     print(json.dumps(out), flush=True)

@@ -82,6 +82,63 @@ def evict_at_layout(L: int, p: int, w: int, s: int, strategy: str = "keep_all") 
     return np.minimum(e, L).astype(np.int32)
 
 
+def reprefill_traces(L: int, p: int, w: int, s: int, strategy: str = "keep_all") -> List[np.ndarray]:
+    """The fresh traces that re-prefill compaction runs for the same rollout
+    (Section 2, "Prefill-compaction"; Appendix E).
+
+    Without KV-streams every compaction continues in a new trace that first
+    re-processes the entries the compaction keeps (the prompt and the retained
+    summaries, with reset positions) and then holds the next segment.  Trace 0
+    is the prompt plus segment 0; trace ``k >= 1`` is the prompt, the summaries
+    retained by compaction ``k - 1`` under the strategy, then segment ``k``
+    (clipped at ``L``).  Every trace is plain causal attention.  Returns, per
+    trace, the original token index of each position.
+    """
+    if strategy not in STRATEGIES:
+        raise ValueError(f"unknown strategy {strategy!r}")
+    if L <= p or w + s <= 0:
+        return [np.arange(L, dtype=np.int64)]
+    a = segment_starts(L, p, w, s)
+    prompt = np.arange(p, dtype=np.int64)
+    traces = []
+    k = 0
+    while a[k] < L:
+        new = np.arange(a[k], min(a[k + 1], L), dtype=np.int64)
+        if k == 0:
+            traces.append(np.concatenate([prompt, new]))
+        else:
+            if strategy == "keep_all":
+                keep = range(0, k)
+            elif strategy == "latest_only":
+                keep = range(k - 1, k)
+            else:
+                keep = range(max(k - 2, 0), k)
+            summ = [np.arange(a[c] + w, a[c + 1], dtype=np.int64) for c in keep]
+            traces.append(np.concatenate([prompt] + summ + [new]))
+        if a[k + 1] > L:   # the last segment's summary is cut off: no further compaction
+            break
+        k += 1
+    return traces
+
+
+def reprefill_extra_tokens(L: int, p: int, w: int, s: int, strategy: str = "keep_all") -> dict:
+    """Extra prefilled entries of re-prefill compaction: the exact count for the
+    layout (sum of the trace lengths minus ``L``) and the estimate
+    ``N r / (B - r)`` of Section 2 (Appendix E), taking ``N = L - p`` generated
+    entries, ``B - r = w + s`` new entries between compactions and ``r`` the
+    mean number of kept entries over the traces that re-prefill them."""
+    tr = reprefill_traces(L, p, w, s, strategy)
+    exact = int(sum(len(t) for t in tr)) - L
+    kept = []
+    a = segment_starts(L, p, w, s) if L > p and w + s > 0 else [p]
+    for k in range(1, len(tr)):
+        kept.append(len(tr[k]) - (min(a[k + 1], L) - a[k]))
+    r = float(np.mean(kept)) if kept else 0.0
+    formula = (L - p) * r / (w + s) if kept else 0.0
+    return {"traces": len(tr), "tokens": int(sum(len(t) for t in tr)), "extra_exact": exact,
+            "kept_mean": r, "extra_formula": formula}
+
+
 def evict_at_random(L: int, rng: np.random.Generator, p_never: float = 0.3) -> np.ndarray:
     """Unstructured valid eviction indices: ``e_j`` uniform on ``(j, L]`` (``L`` = never)."""
     e = np.empty(L, dtype=np.int64)

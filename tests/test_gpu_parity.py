@@ -103,6 +103,17 @@ def test_long_key_spans_split_varlen(kvs):
     _parity(kvs, wl, wl.evict_at(), cu=wl.cu_seqlens())
 
 
+# The re-prefill baseline (the fresh causal traces re-prefill compaction runs
+# for the same rollout) goes through the same library as a varlen batch with
+# nothing evicted.
+@pytest.mark.parametrize("strategy", ["keep_all", "latest_only", "last2"])
+def test_reprefill_batch(kvs, strategy):
+    lengths = [len(t) for t in inputs.reprefill_traces(700, 33, 97, 13, strategy)]
+    wl = inputs.custom_workload(f"reprefill_{strategy}", 6, 2, 128, lengths, 0, 1, 0, varlen=True, seed=41)
+    e = np.concatenate([np.full(L, L, dtype=np.int32) for L in lengths])
+    _parity(kvs, wl, e, cu=wl.cu_seqlens())
+
+
 def test_self_only_closed_form(kvs):
     # every key lives for one query: O_i = v_i, dQ = dK = 0, dV_j = sum over the group of dO_j
     L, Hq, Hkv, D = 200, 4, 2, 128

@@ -55,3 +55,41 @@ def test_tensors_are_seeded_and_bf16():
         assert str(a[key].dtype) == "torch.bfloat16"
         assert (a[key].view(-1).view(dtype=__import__("torch").int16) == b[key].view(-1).view(dtype=__import__("torch").int16)).all()
     assert a["q"].shape == (40, 4, 16) and a["k"].shape == (40, 2, 16)
+
+
+# ---------------------------------------------------------------- re-prefill baseline traces
+def test_reprefill_tiny_hand_count():
+    # 512 tokens, p=64, w=128, s=32, keep-all: compactions 0 and 1 fire (a_1 = 224, a_2 = 384 <= 512).
+    # trace 0 = [0, 224); trace 1 = prompt 64 + S_0 (32) + [224, 384); trace 2 = prompt + S_0 + S_1 + [384, 512)
+    tr = inputs.reprefill_traces(512, 64, 128, 32, "keep_all")
+    assert [len(t) for t in tr] == [224, 256, 256]
+    assert np.array_equal(tr[1][:96], np.concatenate([np.arange(64), np.arange(192, 224)]))
+    assert np.array_equal(tr[2][:128], np.concatenate([np.arange(64), np.arange(192, 224), np.arange(352, 384)]))
+    ex = inputs.reprefill_extra_tokens(512, 64, 128, 32, "keep_all")
+    assert ex["extra_exact"] == 224 and ex["tokens"] == 736
+
+
+@pytest.mark.parametrize("strategy", inputs.STRATEGIES)
+@pytest.mark.parametrize("L,p,w,s", [(60, 5, 11, 3), (97, 0, 9, 4), (40, 40, 5, 2), (88, 7, 10, 0), (50, 3, 6, 5)])
+def test_reprefill_matches_stream_replay(strategy, L, p, w, s):
+    """Each re-prefill trace starts with exactly the entries the streamed cache
+    holds right after the compaction that opened it, and the new parts of the
+    traces enumerate the rollout once."""
+    import torch
+    from oracle import stream_sim
+
+    q = torch.zeros(L, 1, 4, dtype=torch.float64)
+    kv = torch.zeros(L, 1, 4, dtype=torch.float64)
+    _, _, lives = stream_sim.replay(q, kv, kv, p, w, s, strategy, 1.0, return_live=True)
+    tr = inputs.reprefill_traces(L, p, w, s, strategy)
+    pos = 0   # first token not generated yet
+    for k, t in enumerate(tr):
+        start = int(np.sum(t < pos))   # re-prefilled entries come first, all generated earlier
+        assert np.all(t[:start] < pos) and np.array_equal(t[start:], np.arange(pos, pos + len(t) - start))
+        if k == 0:
+            assert start == 0
+        else:
+            live = [int(j) for j in lives[pos] if j != pos]   # cache right after the compaction, before token pos
+            assert list(t[:start]) == live, (k, list(t[:start]), live)
+        pos += len(t) - start
+    assert pos == L
