@@ -62,11 +62,25 @@ def reprefill_batch(wl):
     from paper_2609_35750_amd import inputs
 
     lengths, extra_exact, extra_formula = [], 0, 0.0
+    e_all, off = wl.evict_at(), 0
     for L in wl.lengths:
-        lengths += [len(t) for t in inputs.reprefill_traces(L, wl.p, wl.w, wl.s, wl.strategy)]
-        ex = inputs.reprefill_extra_tokens(L, wl.p, wl.w, wl.s, wl.strategy)
-        extra_exact += ex["extra_exact"]
-        extra_formula += ex["extra_formula"]
+        tr = inputs.reprefill_traces_from_evict(e_all[off:off + L])
+        off += L
+        lengths += [len(t) for t in tr]
+        extra_exact += sum(len(t) for t in tr) - L
+        # N r / (B - r) (Section 2): N generated entries, r kept and B - r new entries per compaction (means)
+        if len(tr) > 1:
+            # r: entries kept at each compaction; B - r: entries generated between two compactions
+            # (new parts of the traces that end in a compaction; trace 0 minus the prompt if there is one)
+            news, kept = [], []
+            pos = len(tr[0])
+            for t in tr[1:]:
+                k = int(np.sum(t < pos))
+                kept.append(k)
+                news.append(len(t) - k)
+                pos += len(t) - k
+            gaps = news[:-1] if len(news) > 1 else [len(tr[0]) - min(wl.p, L)]
+            extra_formula += (L - wl.p) * float(np.mean(kept)) / float(np.mean(gaps))
     return lengths, extra_exact, extra_formula
 
 

@@ -95,3 +95,59 @@ def live_sets_to_evict_at(lives, L: int) -> np.ndarray:
             raise AssertionError("a deleted key came back")
         present = now
     return e
+
+
+def live_sets_turns(p: int, lengths, strategy: str, window: int, stride: int = 1, picks=None):
+    """Live cache of a turn-level compaction (Section 3; Appendix B), replayed
+    token by token from the strategy's description: the cache holds the prompt
+    and whole turns; right before the first token of a turn that would bring
+    the context above ``window`` turns, a compaction deletes whole turns:
+
+    * ``sliding_window``     the ``stride`` oldest turns;
+    * ``markovian_thinker``  the oldest half (``window // 2`` turns);
+    * ``markovian_pick``     every turn except the chosen ones (``picks[c]``:
+                             positions, oldest first, of the turns kept at
+                             compaction ``c``).
+
+    Returns one sorted array of live token indices per query token."""
+    turns = []     # live turns, oldest first: (turn id, [token indices])
+    prompt = list(range(p))
+    lives = [np.arange(t + 1) for t in range(p)]
+    tok, comp = p, 0
+    for t, n in enumerate(lengths):
+        if len(turns) + 1 > window:
+            if strategy == "sliding_window":
+                turns = turns[stride:]
+            elif strategy == "markovian_thinker":
+                turns = turns[max(window // 2, 1):]
+            elif strategy == "markovian_pick":
+                turns = [turns[i] for i in picks[comp]]
+            else:
+                raise ValueError(strategy)
+            comp += 1
+        turns.append((t, []))
+        for _ in range(n):
+            turns[-1][1].append(tok)
+            live = prompt + [j for (_, toks) in turns for j in toks]
+            lives.append(np.array(sorted(live), dtype=np.int64))
+            tok += 1
+    return lives
+
+
+def attend_live(q, k, v, lives, scale: float):
+    """O [L,Hq,D] and LSE [Hq,L] (torch) of each query over its live key set."""
+    import torch
+
+    L, Hq, D = q.shape
+    G = Hq // k.shape[1]
+    outs, lses = [], []
+    for t in range(L):
+        idx = torch.as_tensor(lives[t], dtype=torch.long)
+        ho, hl = [], []
+        for h in range(Hq):
+            sc = scale * (k[idx, h // G, :] @ q[t, h, :])
+            hl.append(torch.logsumexp(sc, dim=0))
+            ho.append(torch.softmax(sc, dim=0) @ v[idx, h // G, :])
+        outs.append(torch.stack(ho))
+        lses.append(torch.stack(hl))
+    return torch.stack(outs), torch.stack(lses).T

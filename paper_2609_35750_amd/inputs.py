@@ -82,6 +82,98 @@ def evict_at_layout(L: int, p: int, w: int, s: int, strategy: str = "keep_all") 
     return np.minimum(e, L).astype(np.int32)
 
 
+# ---------------------------------------------------------------- turn-level strategies
+# Section 3 ("Markovian Thinker", "Markovian Pick", "Sliding Window") and
+# Appendix B ("Turn-Wise Compaction"): the context holds a prompt (never
+# evicted) and whole turns; compaction removes whole turns and generates no
+# summary.  Turn ``t`` occupies tokens ``[b_t, b_{t+1})`` with ``b_0 = p``.
+# With a budget of ``window`` turns, a compaction fires right before a new
+# turn would make the context exceed the budget:
+#
+# * ``sliding_window``     deletes the oldest ``stride`` turns (Section 3 uses
+#                          stride 1 in the SFT masks, Section 4.3);
+# * ``markovian_thinker``  deletes the oldest half (stride ``window // 2``);
+# * ``markovian_pick``     keeps a chosen subset of ``keep`` turns and
+#                          deletes the others (the choices are an input).
+TURN_STRATEGIES = ("sliding_window", "markovian_thinker", "markovian_pick")
+
+
+def turn_lengths(n: int, lo: int, hi: int, rng: np.random.Generator, pad: int = 1) -> List[int]:
+    """``n`` turn lengths uniform on ``[lo, hi]``, each rounded up to a multiple of
+    ``pad`` (16 mirrors the engine's 16-token KV blocks, Section 4)."""
+    x = rng.integers(lo, hi, n, endpoint=True)
+    return [int(-(-int(v) // pad) * pad) for v in x]
+
+
+def pick_turns(n_turns: int, window: int, keep: int, rng: np.random.Generator) -> List[np.ndarray]:
+    """Random Markovian Pick choices: for every compaction of a rollout of
+    ``n_turns`` turns, the sorted positions (in the current context, oldest
+    first) of the ``keep`` turns that stay."""
+    if not 0 <= keep < window:
+        raise ValueError("keep must be in [0, window)")
+    picks, live = [], 0
+    for _ in range(n_turns):
+        if live == window:
+            picks.append(np.sort(rng.choice(window, size=keep, replace=False)))
+            live = keep
+        live += 1
+    return picks
+
+
+def evict_at_turns(p: int, lengths: Sequence[int], strategy: str, window: int, stride: int = 1,
+                   picks: Optional[Sequence[np.ndarray]] = None) -> np.ndarray:
+    """``evict_at`` (int32, length ``p + sum(lengths)``) of a turn-level compaction."""
+    if strategy not in TURN_STRATEGIES:
+        raise ValueError(f"unknown turn strategy {strategy!r}")
+    if window < 1 or any(x < 1 for x in lengths):
+        raise ValueError("bad turn layout")
+    n = len(lengths)
+    b = np.concatenate([[p], p + np.cumsum(lengths)]).astype(np.int64)   # b[t] = first token of turn t
+    L = int(b[-1])
+    e = np.full(L, L, dtype=np.int64)
+    if strategy in ("sliding_window", "markovian_thinker"):
+        st = max(window // 2, 1) if strategy == "markovian_thinker" else stride
+        if not 1 <= st <= window:
+            raise ValueError("stride must be in [1, window]")
+        # Turn t belongs to deletion group t // st; that group goes with the compaction before turn
+        # (t // st) * st + window (the first turn that would overflow the budget with it still live).
+        for t in range(n):
+            gone = (t // st) * st + window
+            if gone < n:
+                e[b[t]:b[t + 1]] = b[gone]
+    else:
+        if picks is None:
+            raise ValueError("markovian_pick needs the picks")
+        live, c = [], 0
+        for t in range(n):
+            if len(live) == window:
+                kept = [live[i] for i in picks[c]]
+                for u in live:
+                    if u not in kept:
+                        e[b[u]:b[u + 1]] = b[t]
+                live, c = kept, c + 1
+            live.append(t)
+    return np.minimum(e, L).astype(np.int32)
+
+
+def turn_trace(L: int, p: int, strategy: str, window: int, stride: int, keep: int, lo: int, hi: int, pad: int,
+               seed: int, trace: int = 0):
+    """One trace of exactly ``L`` tokens under a turn-level strategy: turn lengths
+    drawn from ``numpy.random.default_rng([seed, trace])`` (the last turn cut at
+    ``L``), picks drawn from the same generator.  Returns ``(evict_at, lengths, picks)``."""
+    rng = np.random.default_rng([seed, trace])
+    lengths, tot = [], p
+    while tot < L:
+        x = turn_lengths(1, lo, hi, rng, pad=pad)[0]
+        x = min(x, L - tot)
+        lengths.append(x)
+        tot += x
+    if not lengths:
+        return np.full(L, L, dtype=np.int32), [], None
+    picks = pick_turns(len(lengths), window, keep, rng) if strategy == "markovian_pick" else None
+    return evict_at_turns(min(p, L), lengths, strategy, window, stride=stride, picks=picks), lengths, picks
+
+
 def reprefill_traces(L: int, p: int, w: int, s: int, strategy: str = "keep_all") -> List[np.ndarray]:
     """The fresh traces that re-prefill compaction runs for the same rollout
     (Section 2, "Prefill-compaction"; Appendix E).
@@ -118,6 +210,24 @@ def reprefill_traces(L: int, p: int, w: int, s: int, strategy: str = "keep_all")
         if a[k + 1] > L:   # the last segment's summary is cut off: no further compaction
             break
         k += 1
+    return traces
+
+
+def reprefill_traces_from_evict(e: np.ndarray) -> List[np.ndarray]:
+    """Re-prefill traces of any single-trace eviction layout: every distinct
+    eviction time ``t < L`` is a compaction; the fresh trace it opens first
+    re-processes the entries generated before ``t`` that are still live after
+    it (``e_j > t``) and then holds the tokens up to the next compaction."""
+    e = np.asarray(e, dtype=np.int64)
+    L = len(e)
+    events = np.unique(e[e < L])
+    events = events[events > 0]
+    bounds = [0] + events.tolist() + [L]
+    traces = [np.arange(0, bounds[1], dtype=np.int64)]
+    for k in range(1, len(bounds) - 1):
+        t = bounds[k]
+        kept = np.nonzero(e[:t] > t)[0]
+        traces.append(np.concatenate([kept, np.arange(t, bounds[k + 1], dtype=np.int64)]))
     return traces
 
 
@@ -163,6 +273,8 @@ class Workload:
     q_prescaled: bool
     varlen: bool
     seed: int
+    # Turn-level layout instead of (w, s) segments: (strategy, window, stride, keep, lo, hi, pad, seed).
+    turns: Optional[tuple] = None
 
     @property
     def B(self) -> int:
@@ -186,6 +298,8 @@ class Workload:
 
     def evict_at(self) -> np.ndarray:
         """Trace-local eviction indices, concatenated in trace order (int32, ``[ntok]``)."""
+        if self.turns is not None:
+            return np.concatenate([turn_trace(L, self.p, *self.turns, trace=b)[0] for b, L in enumerate(self.lengths)])
         return np.concatenate([evict_at_layout(L, self.p, self.w, self.s, self.strategy) for L in self.lengths])
 
     def cu_seqlens(self) -> np.ndarray:
@@ -207,6 +321,10 @@ def _workloads() -> Dict[str, Workload]:
             W("trace32k_latest", 32, 8, 128, (32768,), 1024, 3072, 256, "latest_only", False, False, 1003),
             W("varlen8_gqa5", 40, 8, 128, varlen_lengths(8, 4096, 24576, 39), 512, 2048, 256, "keep_all", False, True, 1004),
             W("trace64k_last2", 64, 8, 128, (65536,), 2048, 2048, 256, "last2", False, False, 1005),
+            # turn-level sliding window (TextWorld-like: 32k tokens, window of 10 turns, stride 1, turns of
+            # 64..1024 tokens padded to 16)
+            W("textworld32k_sliding", 32, 8, 128, (32768,), 1024, 0, 0, "sliding_window", False, False, 1006,
+              ("sliding_window", 10, 1, 0, 64, 1024, 16, 1006)),
         ]
     }
 
@@ -217,10 +335,11 @@ WORKLOAD_ORDER = ["trace512_tiny", "trace16k_gqa4", "trace32k_latest", "varlen8_
 
 def custom_workload(name: str, Hq: int, Hkv: int, D: int, lengths: Sequence[int], p: int, w: int, s: int,
                     strategy: str = "keep_all", q_prescaled: bool = False, varlen: Optional[bool] = None,
-                    seed: int = 0) -> Workload:
+                    seed: int = 0, turns: Optional[tuple] = None) -> Workload:
     if varlen is None:
         varlen = len(lengths) > 1 and len(set(lengths)) > 1
-    return Workload(name, Hq, Hkv, D, tuple(int(x) for x in lengths), p, w, s, strategy, q_prescaled, varlen, seed)
+    return Workload(name, Hq, Hkv, D, tuple(int(x) for x in lengths), p, w, s, strategy, q_prescaled, varlen, seed,
+                    turns)
 
 
 def randn_bf16(shape, seed: int, scale: float = 1.0):

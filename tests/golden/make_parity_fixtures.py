@@ -34,11 +34,16 @@ def sample_positions(wl, rng):
     """Packed token indices: boundaries of the layout in every trace plus random fill."""
     picks = set()
     off = 0
-    for L in wl.lengths:
-        starts = inputs.segment_starts(L, wl.p, wl.w, wl.s)
+    for b, L in enumerate(wl.lengths):
         marks = [0, 1, wl.p - 1, wl.p, L - 2, L - 1]
-        for a in starts[:-1]:
-            marks += [a - 1, a, a + 1, a + wl.w - 1, a + wl.w, a + wl.w + 1]
+        if wl.turns is not None:   # turn boundaries
+            _, lengths, _ = inputs.turn_trace(L, wl.p, *wl.turns, trace=b)
+            for a in np.cumsum([wl.p] + list(lengths))[:-1]:
+                marks += [a - 1, a, a + 1]
+        else:
+            starts = inputs.segment_starts(L, wl.p, wl.w, wl.s)
+            for a in starts[:-1]:
+                marks += [a - 1, a, a + 1, a + wl.w - 1, a + wl.w, a + wl.w + 1]
         for m in marks:
             if 0 <= m < L:
                 picks.add(off + m)

@@ -23,7 +23,7 @@ from tests.gpu_helpers import LSE_ABS, MAX_ABS, REL_L2, announce, assert_close, 
 pytestmark = pytest.mark.gpu
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
-NAMES = ["trace16k_gqa4", "trace32k_latest", "varlen8_gqa5", "trace64k_last2"]
+NAMES = ["trace16k_gqa4", "trace32k_latest", "varlen8_gqa5", "trace64k_last2", "textworld32k_sliding"]
 
 
 @pytest.fixture(scope="module")

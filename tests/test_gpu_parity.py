@@ -114,6 +114,40 @@ def test_reprefill_batch(kvs, strategy):
     _parity(kvs, wl, e, cu=wl.cu_seqlens())
 
 
+# Turn-level strategies of Section 3 (sliding window, Markovian Thinker,
+# Markovian Pick), with and without 16-token turn padding: seeded random
+# layouts (turn lengths, window, stride, picks, head grouping, D), each checked
+# element by element.  Unaligned turn boundaries make most issued tiles PARTIAL.
+def _turn_fuzz_case(seed):
+    rng = np.random.default_rng(1000 + seed)
+    strategy = inputs.TURN_STRATEGIES[seed % 3]
+    window = int(rng.integers(3, 9))
+    stride = int(rng.integers(1, window + 1))
+    keep = int(rng.integers(0, window))
+    lo = int(rng.integers(1, 40))
+    hi = lo + int(rng.integers(0, 150))
+    pad = 16 if seed % 2 else 1
+    L = int(rng.integers(300, 1500))
+    p = int(rng.integers(0, 100))
+    Hq, Hkv = [(4, 4), (8, 2), (6, 3), (10, 2), (8, 1)][seed % 5]
+    D = 128 if seed % 3 != 2 else 64
+    return L, p, Hq, Hkv, D, (strategy, window, stride, keep, lo, hi, pad, 2000 + seed)
+
+
+@pytest.mark.parametrize("seed", range(9))
+def test_turn_strategy_fuzz(kvs, seed):
+    L, p, Hq, Hkv, D, turns = _turn_fuzz_case(seed)
+    wl = inputs.custom_workload(f"turns_{turns[0]}_{seed}", Hq, Hkv, D, [L], p, 0, 0, seed=3000 + seed, turns=turns)
+    _parity(kvs, wl, wl.evict_at())
+
+
+def test_turn_strategy_varlen(kvs):
+    turns = ("markovian_pick", 5, 1, 2, 10, 90, 16, 77)
+    wl = inputs.custom_workload("turns_varlen", 8, 2, 128, [513, 1, 700, 64], 20, 0, 0, varlen=True, seed=78,
+                                turns=turns)
+    _parity(kvs, wl, wl.evict_at(), cu=wl.cu_seqlens())
+
+
 def test_self_only_closed_form(kvs):
     # every key lives for one query: O_i = v_i, dQ = dK = 0, dV_j = sum over the group of dO_j
     L, Hq, Hkv, D = 200, 4, 2, 128

@@ -93,3 +93,31 @@ def test_reprefill_matches_stream_replay(strategy, L, p, w, s):
             assert list(t[:start]) == live, (k, list(t[:start]), live)
         pos += len(t) - start
     assert pos == L
+
+
+@pytest.mark.parametrize("strategy", inputs.STRATEGIES)
+@pytest.mark.parametrize("L,p,w,s", [(512, 64, 128, 32), (60, 5, 11, 3), (97, 0, 9, 4), (88, 7, 10, 0), (16384, 1024, 4096, 512)])
+def test_reprefill_from_evict_matches_layout_builder(strategy, L, p, w, s):
+    """Deriving the fresh traces from evict_at alone gives the segment builder's traces."""
+    a = inputs.reprefill_traces(L, p, w, s, strategy)
+    b = inputs.reprefill_traces_from_evict(inputs.evict_at_layout(L, p, w, s, strategy))
+    assert len(a) == len(b) and all(np.array_equal(x, y) for x, y in zip(a, b))
+
+
+@pytest.mark.parametrize("strategy,window,stride,keep", [("sliding_window", 4, 1, 0), ("markovian_thinker", 6, 0, 0),
+                                                         ("markovian_pick", 5, 0, 2)])
+def test_reprefill_from_evict_turns_match_replay(strategy, window, stride, keep):
+    from oracle import stream_sim
+
+    rng = np.random.default_rng(5)
+    lengths = inputs.turn_lengths(15, 1, 6, rng)
+    picks = inputs.pick_turns(15, window, keep, rng) if strategy == "markovian_pick" else None
+    e = inputs.evict_at_turns(4, lengths, strategy, window, stride=stride, picks=picks)
+    lives = stream_sim.live_sets_turns(4, lengths, strategy, window, stride=stride, picks=picks)
+    pos = 0
+    for k, t in enumerate(inputs.reprefill_traces_from_evict(e)):
+        start = int(np.sum(t < pos))
+        if k:
+            assert list(t[:start]) == [int(j) for j in lives[pos] if j != pos]
+        pos += len(t) - start
+    assert pos == len(e)

@@ -272,3 +272,58 @@ def test_invalid_evict_at_rejected():
     q = _rand((5, 1, 8), 1)
     with pytest.raises(ValueError):
         orc.forward(q, q, q, np.array([1, 2, 2, 5, 5]), 1.0)
+
+
+# ---------------------------------------------------------------- turn-level strategies (Section 3)
+TURN_CASES = [
+    # (p, n_turns, lo, hi, pad, strategy, window, stride, keep, seed)
+    (5, 14, 1, 6, 1, "sliding_window", 4, 1, 0, 1),
+    (0, 20, 2, 5, 1, "sliding_window", 5, 2, 0, 2),
+    (3, 17, 1, 9, 4, "sliding_window", 3, 3, 0, 3),
+    (7, 16, 1, 7, 1, "markovian_thinker", 6, 0, 0, 4),
+    (2, 15, 3, 8, 16, "markovian_thinker", 4, 0, 0, 5),
+    (4, 18, 1, 6, 1, "markovian_pick", 5, 0, 2, 6),
+    (0, 13, 2, 4, 1, "markovian_pick", 3, 0, 1, 7),
+    (6, 12, 1, 5, 2, "markovian_pick", 6, 0, 0, 8),
+]
+
+
+@pytest.mark.parametrize("case", TURN_CASES, ids=lambda c: f"{c[5]}_w{c[6]}_s{c[7]}_k{c[8]}_seed{c[9]}")
+def test_turn_strategies_match_stream_replay(case):
+    """The closed-form eviction indices of the turn-level generators equal the
+    ones implied by an event-driven replay of the streamed cache, and one
+    masked pass of the checker equals attention over the replayed live sets
+    (forward and gradients)."""
+    p, n, lo, hi, pad, strategy, window, stride, keep, seed = case
+    rng = np.random.default_rng(seed)
+    lengths = inputs.turn_lengths(n, lo, hi, rng, pad=pad)
+    picks = inputs.pick_turns(n, window, keep, rng) if strategy == "markovian_pick" else None
+    e = inputs.evict_at_turns(p, lengths, strategy, window, stride=stride, picks=picks)
+    L = len(e)
+    lives = stream_sim.live_sets_turns(p, lengths, strategy, window, stride=stride, picks=picks)
+    assert len(lives) == L
+    np.testing.assert_array_equal(stream_sim.live_sets_to_evict_at(lives, L), e)
+    Hq, Hkv, D = 4, 2, 8
+    q, k, v, do = (inputs.randn_bf16(sh, 300 + seed * 4 + i) for i, sh in
+                   enumerate([(L, Hq, D), (L, Hkv, D), (L, Hkv, D), (L, Hq, D)]))
+    qt, kt, vt = (x.double().clone().requires_grad_(True) for x in (q, k, v))
+    O, LSE = stream_sim.attend_live(qt, kt, vt, lives, 0.4)
+    (O * do.double()).sum().backward()
+    res = orc.backward(q, k, v, e, 0.4, do)
+    np.testing.assert_allclose(res["O"], O.detach().numpy(), rtol=1e-10, atol=1e-10)
+    np.testing.assert_allclose(res["LSE"], LSE.detach().numpy(), rtol=1e-10, atol=1e-10)
+    for key, g in (("dq", qt.grad), ("dk", kt.grad), ("dv", vt.grad)):
+        np.testing.assert_allclose(res[key], g.numpy(), rtol=1e-9, atol=1e-10)
+
+
+def test_turn_padding_and_markovian_thinker_is_half_stride():
+    rng = np.random.default_rng(11)
+    lengths = inputs.turn_lengths(30, 1, 40, rng, pad=16)
+    assert all(x % 16 == 0 and 16 <= x <= 48 for x in lengths)
+    a = inputs.evict_at_turns(10, lengths, "markovian_thinker", 8)
+    b = inputs.evict_at_turns(10, lengths, "sliding_window", 8, stride=4)
+    np.testing.assert_array_equal(a, b)
+    # stride 1: turn t is gone exactly when turn t + window starts
+    c = inputs.evict_at_turns(0, [3] * 10, "sliding_window", 4, stride=1)
+    np.testing.assert_array_equal(c[:18], np.repeat(np.arange(4, 10) * 3, 3))
+    assert np.all(c[18:] == 30)
