@@ -51,15 +51,14 @@ kvs_status_t check_dims(int B, int T, long long ntok, int Hq, int Hkv, int D) {
   return KVS_OK;
 }
 
-// Workgroup shape of the row kernels: HG q-heads (largest divisor of G that
-// is <= 8) times TC chunks of 32 tokens, 4 to 8 waves in all.  Two such
-// workgroups share a CU.
+// Workgroup shape of the row kernels: 4 waves, HG q-heads of one GQA group
+// (4, 2 or 1, whichever divides G) times TC = 4 / HG chunks of 32 tokens, so
+// each K/V tile staged in LDS serves 128 (row, q-head) pairs and two
+// workgroups share a CU whatever the group size.
 void head_grouping(kvs::Problem& p) {
-  int hg = 1;
-  for (int d = 1; d <= 8; ++d)
-    if (p.G % d == 0) hg = d;
+  const int hg = p.G % 4 == 0 ? 4 : (p.G % 2 == 0 ? 2 : 1);
   p.HG = hg;
-  p.TC = hg >= 4 ? 1 : (hg == 3 ? 2 : 4 / hg);
+  p.TC = 4 / hg;
   p.nhg = p.G / hg;
 }
 
