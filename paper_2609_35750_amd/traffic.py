@@ -5,8 +5,8 @@ per dispatch) and the same two passes over a plain device copy of known size
 give the bytes each kernel moves to and from HBM, scaled by what the counters
 read for the copy:
 
-    rocprofv3 --pmc FETCH_SIZE --output-format csv -d OUT/fetch -o run -- python bench.py --no-cpu --steps 2 --warmup 1
-    rocprofv3 --pmc WRITE_SIZE --output-format csv -d OUT/write -o run -- python bench.py --no-cpu --steps 2 --warmup 1
+    rocprofv3 --pmc FETCH_SIZE --output-format csv -d OUT/fetch -o run -- python bench.py --no-cpu --no-reprefill --steps 2 --warmup 1
+    rocprofv3 --pmc WRITE_SIZE --output-format csv -d OUT/write -o run -- python bench.py --no-cpu --no-reprefill --steps 2 --warmup 1
     rocprofv3 --pmc FETCH_SIZE --output-format csv -d OUT/cfetch -o run -- python -m paper_2609_35750_amd.traffic copy
     rocprofv3 --pmc WRITE_SIZE --output-format csv -d OUT/cwrite -o run -- python -m paper_2609_35750_amd.traffic copy
     python -m paper_2609_35750_amd.traffic summarize OUT trace16k_gqa4 profiles
