@@ -258,6 +258,10 @@ def main():
         "roofline": roofline,
     }
     out["value_strict_12D"] = 12 * wl.D * wl.Hq * vis / (ms_per_step * 1e-3) / 1e12   # no recompute counted
+    measured_peak = kvs.kvs_measure_mfma_rate()
+    out["measured_mfma_peak_tflops"] = measured_peak
+    out["pct_of_measured_peak"] = 100.0 * value / measured_peak
+    roofline["frac_of_measured_peak"] = achieved / measured_peak
     if not args.no_reprefill:
         out["reprefill"] = reprefill_compare(wl, kvs, args.warmup, args.steps, ms_per_step)
     if not args.no_cpu:

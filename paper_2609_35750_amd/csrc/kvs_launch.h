@@ -48,6 +48,9 @@ hipError_t launch_classify(const int32_t* evict, const int32_t* cu, int B, int T
 hipError_t launch_check(const int32_t* evict, const int32_t* cu, int B, int T, int ntok,
                         int64_t* first_bad, int* cu_bad, hipStream_t stream);
 
+// Measured dense bf16 MFMA rate of the current device (TFLOP/s); synchronous.
+hipError_t measure_mfma_rate(double* tflops, hipStream_t stream);
+
 // Per-kernel event bracketing (benchmark timing).
 void prof_begin(const char* name, hipStream_t s);
 void prof_end(hipStream_t s);

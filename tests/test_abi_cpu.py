@@ -100,3 +100,7 @@ def test_classify_and_check_validation(kvs):
 def test_prof_read_without_records(kvs):
     kvs.kvs_prof_reset()
     assert kvs.kvs_prof_read("fwd") == (0, 0.0)
+
+
+def test_mfma_rate_probe_validation(kvs):
+    assert kvs.lib.kvs_measure_mfma_rate(None, None) == 1   # KVS_ERR_NULL before any HIP call

@@ -227,3 +227,10 @@ def test_check_evict_at(kvs):
     badcu = torch.tensor([0, 300, 200], dtype=torch.int32, device=dev)
     with pytest.raises(kvs.KvsError):
         kvs.kvs_check_evict_at(torch.from_numpy(e2).to(dev), badcu)
+
+
+def test_mfma_rate_probe(kvs):
+    announce("MFMA rate probe")
+    rate = kvs.kvs_measure_mfma_rate()
+    # attainable dense bf16 rate: positive and not above the published 2516.6 TFLOP/s (2.4 GHz)
+    assert 500.0 < rate <= 2516.6 * 1.02, rate
