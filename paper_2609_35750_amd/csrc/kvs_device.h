@@ -98,7 +98,33 @@ __device__ __forceinline__ uint2 pack4_bf16(float a, float b, float c, float d) 
   return __builtin_bit_cast(uint2, r);
 }
 
-__device__ __forceinline__ float wave_xor32(float x) { return __shfl_xor(x, 32); }
+// Value of lane l ^ 32 (v_permlane32_swap: a VALU exchange of the two wave halves).
+__device__ __forceinline__ float wave_xor32(float x) {
+  // swap(x, x): first result = low half of x in both halves, second = high half in both
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float((threadIdx.x & 32) ? r[0] : r[1]);
+}
+// max and sum of x over lanes l and l ^ 32
+__device__ __forceinline__ float halves_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float halves_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// acc + sum of the eight bf16 values of p (v_dot2 with ones: two values per instruction)
+__device__ __forceinline__ float add_bf16x8(float acc, bf16x8 p) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  const bf16x2 one = {(__bf16)1.f, (__bf16)1.f};
+#pragma unroll
+  for (int e = 0; e < 8; e += 2) {
+    const bf16x2 v = {p[e], p[e + 1]};
+    acc = __builtin_amdgcn_fdot2_f32_bf16(v, one, acc, false);
+  }
+  return acc;
+}
 
 // Asynchronous global -> LDS copy (global_load_lds_dword{,x4}): lane l of the
 // wave writes its 4 or 16 bytes at LDS byte address lds + (4 or 16) l.  Issued

@@ -263,19 +263,31 @@ __device__ __forceinline__ void stage_kv(const KVStager<D>& st, uint16_t* sK, ui
 }
 
 // ---------------------------------------------------------------- forward
-// The K/V tiles are double-buffered in two distinct LDS arrays each; the loop
-// body alternates between them so the compiler can tell that the
-// asynchronous fill of the next buffer never aliases the reads of the
-// current one (and does not wait for the fill before reading).
+// K/V are staged in sub-tiles of BN keys (D = 128: 32, so that a workgroup
+// needs 37 KB of LDS and three workgroups share a CU; D = 64: 64), walked in
+// the order of the non-EMPTY 64-key tiles.  The sub-tiles are double-buffered
+// in two distinct LDS arrays each; the loop body alternates between them so
+// the compiler can tell that the asynchronous fill of the next buffer never
+// aliases the reads of the current one (and does not wait for the fill
+// before reading).  A sub-tile's class comes from the statistics of its
+// 64-key tile, which can only report PARTIAL where FULL would hold or
+// non-EMPTY where EMPTY would: a conservative, exact choice.
 template <int D>
-__global__ void __launch_bounds__(512) fwd_kernel(RowArgs a) {
-  constexpr int KS = D / 16, DB = D / 32;
-  __shared__ __attribute__((aligned(1024))) uint16_t sK0[kKeyTile * Lay<D>::PITCH];
-  __shared__ __attribute__((aligned(1024))) uint16_t sK1[kKeyTile * Lay<D>::PITCH];
-  __shared__ __attribute__((aligned(1024))) uint16_t sV0[kKeyTile * Lay<D>::PITCH];
-  __shared__ __attribute__((aligned(1024))) uint16_t sV1[kKeyTile * Lay<D>::PITCH];
-  __shared__ __attribute__((aligned(256))) int sE0[kKeyTile];
-  __shared__ __attribute__((aligned(256))) int sE1[kKeyTile];
+constexpr int fwd_bn() { return D == 128 ? 32 : 64; }
+
+template <int D>
+using FwdStager = RowStager<D, fwd_bn<D>(), (fwd_bn<D>() * Lay<D>::CPRP / kWave + 3) / 4>;   // >= 4 waves
+
+template <int D>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 128 ? 3 : 2, D == 128 ? 3 : 2)))
+fwd_kernel(RowArgs a) {
+  constexpr int KS = D / 16, DB = D / 32, BN = fwd_bn<D>(), NKB = BN / 32, NSUB = kKeyTile / BN;
+  __shared__ __attribute__((aligned(1024))) uint16_t sK0[BN * Lay<D>::PITCH];
+  __shared__ __attribute__((aligned(1024))) uint16_t sK1[BN * Lay<D>::PITCH];
+  __shared__ __attribute__((aligned(1024))) uint16_t sV0[BN * Lay<D>::PITCH];
+  __shared__ __attribute__((aligned(1024))) uint16_t sV1[BN * Lay<D>::PITCH];
+  __shared__ __attribute__((aligned(256))) int sE0[BN];
+  __shared__ __attribute__((aligned(256))) int sE1[BN];
 
   RowTile rt;
   if (!row_tile(a, rt)) return;
@@ -285,8 +297,19 @@ __global__ void __launch_bounds__(512) fwd_kernel(RowArgs a) {
   const int i = rt.i0w + col;
   const bool row_ok = i < tr.L;
   const int rl = Lay<D>::row_lane(lane), tl = Lay<D>::tr_lo(lane), th = Lay<D>::tr_hi(lane);
-  KVStager<D> kvst;
+  FwdStager<D> kvst;
   kvst.init(wave, nw, lane, (long long)a.Hkv * D);
+  // asynchronous staging of sub-tile (kt, sub) of KV head g
+  auto stage = [&](uint16_t* sK, uint16_t* sV, int* sE, int kt, int sub) __attribute__((always_inline)) {
+    const int j0 = kt * kKeyTile + sub * BN;
+    const long long base = ((long long)rt.tr.tok0 * a.Hkv + rt.g) * D;
+    const long long stride = (long long)a.Hkv * D;
+    kvst.issue(lds_addr(sK), a.k + base, stride, j0, rt.tr.L - 1, wave, nw);
+    kvst.issue(lds_addr(sV), a.v + base, stride, j0, rt.tr.L - 1, wave, nw);
+    if (wave == nw - 1) {
+      if (BN == kWave || lane < BN) stage_words(lds_addr(sE), a.evict + rt.tr.tok0, j0, rt.tr.L - 1, lane);
+    }
+  };
 
   bf16x8 qreg[KS];
   {
@@ -305,29 +328,34 @@ __global__ void __launch_bounds__(512) fwd_kernel(RowArgs a) {
   walker_load(w, a.kstats, kidx0, rt.i0, rt.i1, tr.L);
   int kt = __builtin_amdgcn_readfirstlane(walker_next(w, a.kstats, kidx0, rt.i0, rt.i1, tr.L));
   int2 kst = kt >= 0 ? a.kstats[kidx0 + kt] : make_int2(0, 0);
+  int sub = 0;
 
   // One tile: prefetch the next tile into (nK, nV, nE), compute on (cK, cV, cE).
   auto body = [&](const uint16_t* cK, const uint16_t* cV, const int* cE, uint16_t* nK, uint16_t* nV, int* nE) {
     // Statistics of the next tile are read before its copy is issued and used one
     // iteration later, so no wait on this iteration's copies is needed for them.
-    const int nkt = __builtin_amdgcn_readfirstlane(walker_next(w, a.kstats, kidx0, rt.i0, rt.i1, tr.L));
-    int2 nkst = make_int2(0, 0);
-    if (nkt >= 0) {
-      nkst = a.kstats[kidx0 + nkt];
-      stage_kv<D>(kvst, nK, nV, nE, a, rt, nkt, wave, nw, lane);
+    int nkt = kt, nsub = sub + 1;
+    int2 nkst = kst;
+    // next 64-key tile once this one is done or its remaining keys lie past the trace end
+    // (a staged sub-tile must start inside the trace)
+    if (nsub == NSUB || kt * kKeyTile + nsub * BN >= tr.L) {
+      nkt = __builtin_amdgcn_readfirstlane(walker_next(w, a.kstats, kidx0, rt.i0, rt.i1, tr.L));
+      nsub = 0;
+      if (nkt >= 0) nkst = a.kstats[kidx0 + nkt];
     }
-    const int j0 = kt * kKeyTile;
-    const int cls = tile_class(rt.i0w, rt.i0w + 32, j0, j0 + kKeyTile, tr.L, kst.x, kst.y);
+    if (nkt >= 0) stage(nK, nV, nE, nkt, nsub);
+    const int j0 = kt * kKeyTile + sub * BN;
+    const int cls = tile_class(rt.i0w, rt.i0w + 32, j0, j0 + BN, tr.L, kst.x, kst.y);
     if (cls != kEmpty) {
-      f32x16 s[2];
+      f32x16 s[NKB];
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
+      for (int kb = 0; kb < NKB; ++kb) {
         s[kb] = scores_t<D>(cK, 32 * kb, qreg, rl);
         if (cls == kPartial) mask_t(s[kb], cE, kb, j0, i, tr.L, half);
       }
       float mx = -INFINITY;
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+      for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
       mx = fmaxf(mx, wave_xor32(mx)) * a.scale_log2;
@@ -347,7 +375,7 @@ __global__ void __launch_bounds__(512) fwd_kernel(RowArgs a) {
       const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
       float ls = 0.f;
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+      for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][r], a.scale_log2, -m_use));
@@ -356,7 +384,7 @@ __global__ void __launch_bounds__(512) fwd_kernel(RowArgs a) {
         }
       l_run += ls;
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+      for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
           const bf16x8 pb = pack8(s[kb], 8 * t);
@@ -368,10 +396,11 @@ __global__ void __launch_bounds__(512) fwd_kernel(RowArgs a) {
     wait_vm();
     __syncthreads();
     kt = nkt;
+    sub = nsub;
     kst = nkst;
   };
 
-  if (kt >= 0) stage_kv<D>(kvst, sK0, sV0, sE0, a, rt, kt, wave, nw, lane);
+  if (kt >= 0) stage(sK0, sV0, sE0, kt, 0);
   wait_vm();
   __syncthreads();
   while (kt >= 0) {
@@ -1195,7 +1224,7 @@ hipError_t launch_kstats(const Problem& p, int BN, int2* kstats) {
 hipError_t launch_fwd(const Problem& p, const int2* kstats) {
   RowArgs a = row_args(p, kstats);
   const long long nblk = (long long)a.nqt * p.B * p.Hkv * p.nhg;
-  dim3 grid((unsigned)nblk), block(64 * p.HG * p.TC);
+  dim3 grid((unsigned)nblk), block(64 * p.HG * p.TC);   // 4 waves
   prof_begin("fwd", p.stream);
   if (p.D == 128) hipLaunchKernelGGL(fwd_kernel<128>, grid, block, 0, p.stream, a);
   else hipLaunchKernelGGL(fwd_kernel<64>, grid, block, 0, p.stream, a);
