@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define KVS_ABI_VERSION 1
+#define KVS_ABI_VERSION 2
 
 typedef enum {
   KVS_OK = 0,
@@ -65,7 +65,9 @@ typedef enum {
   KVS_ERR_WORKSPACE = 4,    /* workspace smaller than the *_workspace query */
   KVS_ERR_EVICT = 5,        /* invalid evict_at (only kvs_check_evict_at reports it) */
   KVS_ERR_HIP = 6,          /* a HIP launch or runtime call failed; see kvs_last_error() */
-  KVS_ERR_UNSUPPORTED = 7   /* valid but outside the supported limits above */
+  KVS_ERR_UNSUPPORTED = 7,  /* valid but outside the supported limits above */
+  KVS_ERR_CAPACITY = 8,     /* paged cache: no free block, or a sequence's block table is full */
+  KVS_ERR_STATE = 9         /* paged cache: position already cached, or not cached */
 } kvs_status_t;
 
 /* ABI version of the loaded library (KVS_ABI_VERSION it was built with). */
@@ -152,8 +154,8 @@ kvs_status_t kvs_check_evict_at(const int32_t* evict_at, const int32_t* cu_seqle
  * Per-kernel timing for benchmarks.  While enabled, each call brackets every
  * kernel it launches with HIP events on the call's stream.  kvs_prof_read
  * waits for the recorded events and returns, for the kernel named `name`
- * ("classify", "fwd", "bwd_pre", "bwd_dkdv", "bwd_dq"), the number of
- * launches and their total duration in milliseconds.  Not thread-safe;
+ * ("classify", "fwd", "bwd_pre", "bwd_dkdv", "bwd_dq", "paged_decode"), the
+ * number of launches and their total duration in milliseconds.  Not thread-safe;
  * meant for single-threaded benchmark drivers.
  */
 void kvs_prof_enable(int on);
@@ -168,6 +170,99 @@ kvs_status_t kvs_prof_read(const char* name, int* launches, double* total_ms);
  * published peak (256 CU x 2.4 GHz x 4096 FLOP/clk).  Synchronous.  Returns
  * KVS_ERR_NULL for a NULL tflops and KVS_ERR_HIP on a launch or event error. */
 kvs_status_t kvs_measure_mfma_rate(double* tflops, void* stream);
+
+/* ================================================================ streamed paged KV cache
+ * The inference side of KV-streams (Section 2, "KV-streams"; Section 4,
+ * "Inference engine implementation"): the engine appends one (K, V) entry per
+ * generated token to a paged cache, evicts entries directly in the cache when
+ * a compaction fires (they never come back), and each query attends over
+ * exactly the entries that are live when it is generated.  Decoding token i
+ * of a trace therefore computes row i of the eviction-masked attention above
+ * (keys j <= i with evict_at[j] > i), which is what lets the trainer replay a
+ * whole rollout in one masked pass.  Block sizes: 16 (the vLLM setup, turns
+ * padded to 16 tokens) or 1 (the SGLang setup); any size in [1, 64] works.
+ *
+ * Device cache (caller-owned, allocated once):
+ *   K_cache, V_cache  bf16 [num_blocks][block_size][Hkv][D]  (16-byte aligned)
+ *   slot_pos          int32 [num_blocks * block_size]: trace position of the
+ *                     token held by each slot, -1 for an empty or evicted slot.
+ *                     Must be filled with -1 before first use.
+ * Host bookkeeping: a block manager (kvs_bm_*) hands out slots, drops
+ * evicted entries, frees blocks with no live entry and produces the block
+ * tables the decode call reads:
+ *   block_table  int32 [num_seqs][max_blocks]: a sequence's blocks in
+ *                allocation order (entries past seq_blocks[s] are ignored)
+ *   seq_blocks   int32 [num_seqs]
+ * A slot of a block stays allocated until the whole block is free, so the
+ * decode call masks the evicted slots of partly evicted blocks by slot_pos.
+ */
+
+/* ---- host block manager (host memory only; not thread-safe; no HIP calls) */
+typedef struct kvs_block_manager kvs_block_manager;
+
+/* New manager of num_blocks cache blocks of block_size slots for num_seqs
+ * sequences of at most max_blocks blocks each (*out, host).  KVS_ERR_SHAPE for
+ * non-positive sizes or block_size > 64, KVS_ERR_UNSUPPORTED if
+ * num_blocks * block_size exceeds INT32_MAX. */
+kvs_status_t kvs_bm_create(int num_blocks, int block_size, int num_seqs, int max_blocks,
+                           kvs_block_manager** out);
+void kvs_bm_destroy(kvs_block_manager* bm);
+
+/* Reserve slots for n tokens of sequence seq at trace positions pos[0..n)
+ * (host arrays); slots[i] receives the slot of pos[i].  Tokens fill the tail
+ * of the sequence's last block, then fresh blocks.  All-or-nothing:
+ * KVS_ERR_CAPACITY (no free block / table full) or KVS_ERR_STATE (a position
+ * already cached or repeated) leave the manager unchanged. */
+kvs_status_t kvs_bm_append(kvs_block_manager* bm, int seq, const int32_t* pos, int n, int32_t* slots);
+
+/* Evict the entries of sequence seq at trace positions pos[0..n); slots[i]
+ * receives the slot that held pos[i] (pass them to kvs_paged_evict).  Blocks
+ * left without a live entry return to the free list and leave the sequence's
+ * table.  All-or-nothing; KVS_ERR_STATE if a position is not cached or repeated. */
+kvs_status_t kvs_bm_evict(kvs_block_manager* bm, int seq, const int32_t* pos, int n, int32_t* slots);
+
+/* Drop sequence seq entirely: writes its live slots (sorted; `slots` must hold
+ * kvs_bm_live(bm, seq) entries) and their count, and frees all its blocks. */
+kvs_status_t kvs_bm_release(kvs_block_manager* bm, int seq, int32_t* slots, int* n_slots);
+
+/* Host copies of block_table [num_seqs][max_blocks] (unused entries 0) and seq_blocks [num_seqs]. */
+kvs_status_t kvs_bm_tables(const kvs_block_manager* bm, int32_t* block_table, int32_t* seq_blocks);
+
+/* Free blocks; live entries of sequence seq (-1 for a bad index or NULL manager). */
+int kvs_bm_free_blocks(const kvs_block_manager* bm);
+int kvs_bm_live(const kvs_block_manager* bm, int seq);
+
+/* ---- device updates (enqueued on `stream`) */
+
+/* Write n new tokens into the cache: K_new, V_new bf16 [n][Hkv][D] go to
+ * slots[0..n) of K_cache, V_cache and slot_pos[slots[t]] = positions[t]
+ * (positions, slots: device int32 [n]).  Slots outside [0, num_blocks *
+ * block_size) are skipped (the device cannot report them). */
+kvs_status_t kvs_paged_append(const void* K_new, const void* V_new, const int32_t* positions,
+                              const int32_t* slots, int n, void* K_cache, void* V_cache, int32_t* slot_pos,
+                              int num_blocks, int block_size, int Hkv, int D, void* stream);
+
+/* Mark slots[0..n) (device int32) evicted: slot_pos = -1.  Out-of-range slots are skipped. */
+kvs_status_t kvs_paged_evict(const int32_t* slots, int n, int32_t* slot_pos, int num_blocks, int block_size,
+                             void* stream);
+
+/* ---- decode attention over the live cache
+ * One query token per sequence: Q, O bf16 [num_seqs][Hq][D], LSE fp32
+ * [num_seqs][Hq] (natural log).  Sequence s attends over every slot of its
+ * first seq_blocks[s] table blocks whose slot_pos is >= 0, with q-head h on KV
+ * head h / (Hq / Hkv).  A sequence with no live slot gets O = 0, LSE = -inf.
+ * Device inputs that the host cannot see are clamped, never trusted for
+ * addressing: seq_blocks to [0, max_blocks]; a table entry outside
+ * [0, num_blocks) reads nothing and counts as evicted.
+ * Supported: D in {64, 128}; Hq / Hkv <= 32; block_size in [1, 64];
+ * num_blocks * block_size <= INT32_MAX.  Workspace: fp32 partials of the
+ * key splits (size from the query below, 256-byte aligned). */
+size_t kvs_paged_decode_workspace(int num_seqs, int Hq, int Hkv, int D, int max_blocks, int block_size);
+kvs_status_t kvs_paged_decode(const void* Q, const void* K_cache, const void* V_cache, const int32_t* slot_pos,
+                              const int32_t* block_table, const int32_t* seq_blocks, void* O, float* LSE,
+                              int num_seqs, int Hq, int Hkv, int D, int num_blocks, int block_size,
+                              int max_blocks, float softmax_scale, void* workspace, size_t workspace_bytes,
+                              void* stream);
 
 #ifdef __cplusplus
 }

@@ -11,6 +11,9 @@ baseline leg of the benchmark may import it; the library never calls it.
                   token by token (Section 2, "Compaction" and "KV-streams";
                   Section 3, "Summary").
 * ``tiles``       per-element counting classifier for Q x K tiles.
+* ``paged``       decode attention of one query over the live entries of a
+                  streamed KV cache (Section 2, "KV-streams": the inference
+                  engine evicts entries in place).
 
 Numbers are fp64 (the paper fixes no precision for this computation).
 Shares no code with the HIP path.

@@ -38,7 +38,7 @@ def build(verbose: bool = False) -> str:
     objdir = os.path.join(ROOT, "_build")
     os.makedirs(objdir, exist_ok=True)
     objs = []
-    for src in ("kvs_kernels.hip", "kvs_api.cpp"):
+    for src in ("kvs_kernels.hip", "kvs_paged.hip", "kvs_api.cpp", "kvs_cache.cpp"):
         obj = os.path.join(objdir, src + ".o")
         lang = ["-x", "hip"] if src.endswith(".hip") else []
         cmd = [hipcc, *HIP_FLAGS, *lang, "-I", INCLUDE, "-I", CSRC, "-c", os.path.join(CSRC, src), "-o", obj]

@@ -11,6 +11,7 @@
 #include <string>
 #include <vector>
 
+#include "kvs_cache.h"
 #include "kvs_launch.h"
 
 namespace {
@@ -152,6 +153,8 @@ const char* kvs_status_string(kvs_status_t s) {
     case KVS_ERR_EVICT: return "invalid evict_at (some evict_at[j] <= j)";
     case KVS_ERR_HIP: return "HIP runtime error";
     case KVS_ERR_UNSUPPORTED: return "unsupported configuration";
+    case KVS_ERR_CAPACITY: return "paged cache capacity exceeded";
+    case KVS_ERR_STATE: return "paged cache state conflict";
   }
   return "unknown status";
 }
@@ -343,6 +346,170 @@ kvs_status_t kvs_prof_read(const char* name, int* launches, double* total_ms) {
   *launches = n;
   *total_ms = tot;
   return KVS_OK;
+}
+
+// ---------------------------------------------------------------- streamed paged KV cache
+struct kvs_block_manager {
+  kvs::BlockManager impl;
+};
+
+static kvs_status_t bm_status(int code, const std::string& msg) {
+  switch (code) {
+    case kvs::BlockManager::kOk: return KVS_OK;
+    case kvs::BlockManager::kBadArg: return fail(KVS_ERR_SHAPE, "%s", msg.c_str());
+    case kvs::BlockManager::kBadState: return fail(KVS_ERR_STATE, "%s", msg.c_str());
+    default: return fail(KVS_ERR_CAPACITY, "%s", msg.c_str());
+  }
+}
+
+kvs_status_t kvs_bm_create(int num_blocks, int block_size, int num_seqs, int max_blocks, kvs_block_manager** out) {
+  t_err.clear();
+  if (!out) return fail(KVS_ERR_NULL, "out is NULL");
+  *out = nullptr;
+  if (num_blocks < 1 || block_size < 1 || num_seqs < 1 || max_blocks < 1)
+    return fail(KVS_ERR_SHAPE, "num_blocks, block_size, num_seqs, max_blocks must be >= 1");
+  if (block_size > 64) return fail(KVS_ERR_SHAPE, "block_size %d above 64", block_size);
+  if ((long long)num_blocks * block_size > 0x7fffffffll)
+    return fail(KVS_ERR_UNSUPPORTED, "num_blocks * block_size above INT32_MAX");
+  *out = new kvs_block_manager{kvs::BlockManager(num_blocks, block_size, num_seqs, max_blocks)};
+  return KVS_OK;
+}
+
+void kvs_bm_destroy(kvs_block_manager* bm) { delete bm; }
+
+kvs_status_t kvs_bm_append(kvs_block_manager* bm, int seq, const int32_t* pos, int n, int32_t* slots) {
+  t_err.clear();
+  if (!bm) return fail(KVS_ERR_NULL, "block manager is NULL");
+  if (n < 0) return fail(KVS_ERR_SHAPE, "n must be >= 0");
+  if (n > 0 && (!pos || !slots)) return fail(KVS_ERR_NULL, "pos or slots is NULL");
+  std::string msg;
+  return bm_status(bm->impl.append(seq, pos, n, slots, &msg), msg);
+}
+
+kvs_status_t kvs_bm_evict(kvs_block_manager* bm, int seq, const int32_t* pos, int n, int32_t* slots) {
+  t_err.clear();
+  if (!bm) return fail(KVS_ERR_NULL, "block manager is NULL");
+  if (n < 0) return fail(KVS_ERR_SHAPE, "n must be >= 0");
+  if (n > 0 && (!pos || !slots)) return fail(KVS_ERR_NULL, "pos or slots is NULL");
+  std::string msg;
+  return bm_status(bm->impl.evict(seq, pos, n, slots, &msg), msg);
+}
+
+kvs_status_t kvs_bm_release(kvs_block_manager* bm, int seq, int32_t* slots, int* n_slots) {
+  t_err.clear();
+  if (!bm || !n_slots) return fail(KVS_ERR_NULL, "block manager or n_slots is NULL");
+  if (bm->impl.live(seq) > 0 && !slots) return fail(KVS_ERR_NULL, "slots is NULL");
+  std::string msg;
+  return bm_status(bm->impl.release(seq, slots, n_slots, &msg), msg);
+}
+
+kvs_status_t kvs_bm_tables(const kvs_block_manager* bm, int32_t* block_table, int32_t* seq_blocks) {
+  t_err.clear();
+  if (!bm || !block_table || !seq_blocks) return fail(KVS_ERR_NULL, "NULL argument");
+  bm->impl.tables(block_table, seq_blocks);
+  return KVS_OK;
+}
+
+int kvs_bm_free_blocks(const kvs_block_manager* bm) { return bm ? bm->impl.free_blocks() : -1; }
+int kvs_bm_live(const kvs_block_manager* bm, int seq) { return bm ? bm->impl.live(seq) : -1; }
+
+static kvs_status_t check_cache_dims(int num_blocks, int block_size) {
+  if (num_blocks < 1 || block_size < 1 || block_size > 64)
+    return fail(KVS_ERR_SHAPE, "num_blocks must be >= 1 and block_size in [1, 64]");
+  if ((long long)num_blocks * block_size > 0x7fffffffll)
+    return fail(KVS_ERR_UNSUPPORTED, "num_blocks * block_size above INT32_MAX");
+  return KVS_OK;
+}
+
+kvs_status_t kvs_paged_append(const void* K_new, const void* V_new, const int32_t* positions, const int32_t* slots,
+                              int n, void* K_cache, void* V_cache, int32_t* slot_pos, int num_blocks,
+                              int block_size, int Hkv, int D, void* stream) {
+  t_err.clear();
+  if (kvs_status_t st = check_cache_dims(num_blocks, block_size)) return st;
+  if (n < 0 || Hkv < 1) return fail(KVS_ERR_SHAPE, "n must be >= 0 and Hkv >= 1");
+  if (D != 64 && D != 128) return fail(KVS_ERR_SHAPE, "head dim D must be 64 or 128 (got %d)", D);
+  REQUIRE_PTR(K_cache, "K_cache");
+  REQUIRE_PTR(V_cache, "V_cache");
+  if (!slot_pos) return fail(KVS_ERR_NULL, "slot_pos is NULL");
+  if (n == 0) return KVS_OK;
+  REQUIRE_PTR(K_new, "K_new");
+  REQUIRE_PTR(V_new, "V_new");
+  if (!positions || !slots) return fail(KVS_ERR_NULL, "positions or slots is NULL");
+  hipError_t e = kvs::launch_paged_append(K_new, V_new, positions, slots, n, K_cache, V_cache, slot_pos,
+                                          num_blocks * block_size, Hkv, D, (hipStream_t)stream);
+  return e == hipSuccess ? KVS_OK : hip_fail(e, "paged append launch");
+}
+
+kvs_status_t kvs_paged_evict(const int32_t* slots, int n, int32_t* slot_pos, int num_blocks, int block_size,
+                             void* stream) {
+  t_err.clear();
+  if (kvs_status_t st = check_cache_dims(num_blocks, block_size)) return st;
+  if (n < 0) return fail(KVS_ERR_SHAPE, "n must be >= 0");
+  if (!slot_pos) return fail(KVS_ERR_NULL, "slot_pos is NULL");
+  if (n == 0) return KVS_OK;
+  if (!slots) return fail(KVS_ERR_NULL, "slots is NULL");
+  hipError_t e = kvs::launch_paged_evict(slots, n, slot_pos, num_blocks * block_size, (hipStream_t)stream);
+  return e == hipSuccess ? KVS_OK : hip_fail(e, "paged evict launch");
+}
+
+static kvs_status_t check_decode_dims(int S, int Hq, int Hkv, int D, int num_blocks, int block_size,
+                                      int max_blocks) {
+  if (S < 1 || Hq < 1 || Hkv < 1 || max_blocks < 1)
+    return fail(KVS_ERR_SHAPE, "num_seqs, Hq, Hkv, max_blocks must be >= 1");
+  if (Hq % Hkv != 0) return fail(KVS_ERR_SHAPE, "Hq (%d) must be a multiple of Hkv (%d)", Hq, Hkv);
+  if (D != 64 && D != 128) return fail(KVS_ERR_SHAPE, "head dim D must be 64 or 128 (got %d)", D);
+  if (kvs_status_t st = check_cache_dims(num_blocks, block_size)) return st;
+  if (Hq / Hkv > 32) return fail(KVS_ERR_UNSUPPORTED, "decode supports GQA groups of at most 32 (got %d)", Hq / Hkv);
+  if ((long long)max_blocks * block_size > 0x7fffffffll)
+    return fail(KVS_ERR_UNSUPPORTED, "max_blocks * block_size above INT32_MAX");
+  if ((long long)S * Hkv * kvs::paged_nsplit(max_blocks, block_size, kvs::paged_split_slots(S, Hkv, max_blocks, block_size)) >
+      0x7fffffffll)
+    return fail(KVS_ERR_UNSUPPORTED, "decode grid too large");
+  return KVS_OK;
+}
+
+size_t kvs_paged_decode_workspace(int num_seqs, int Hq, int Hkv, int D, int max_blocks, int block_size) {
+  if (num_seqs < 1 || Hkv < 1 || max_blocks < 1 || block_size < 1) return 0;
+  const int per = kvs::paged_split_slots(num_seqs, Hkv, max_blocks, block_size);
+  return kvs::paged_ws_bytes(num_seqs, Hq, D, kvs::paged_nsplit(max_blocks, block_size, per));
+}
+
+kvs_status_t kvs_paged_decode(const void* Q, const void* K_cache, const void* V_cache, const int32_t* slot_pos,
+                              const int32_t* block_table, const int32_t* seq_blocks, void* O, float* LSE,
+                              int num_seqs, int Hq, int Hkv, int D, int num_blocks, int block_size, int max_blocks,
+                              float softmax_scale, void* workspace, size_t workspace_bytes, void* stream) {
+  t_err.clear();
+  if (kvs_status_t st = check_decode_dims(num_seqs, Hq, Hkv, D, num_blocks, block_size, max_blocks)) return st;
+  if (!(softmax_scale > 0.f) || softmax_scale != softmax_scale)
+    return fail(KVS_ERR_SHAPE, "softmax_scale must be positive and finite");
+  REQUIRE_PTR(Q, "Q");
+  REQUIRE_PTR(K_cache, "K_cache");
+  REQUIRE_PTR(V_cache, "V_cache");
+  REQUIRE_PTR(O, "O");
+  if (!slot_pos || !block_table || !seq_blocks || !LSE) return fail(KVS_ERR_NULL, "NULL table or output pointer");
+  const size_t need = kvs_paged_decode_workspace(num_seqs, Hq, Hkv, D, max_blocks, block_size);
+  if (kvs_status_t st = check_ws(workspace, workspace_bytes, need)) return st;
+  kvs::PagedDecode p{};
+  p.q = Q;
+  p.k_cache = K_cache;
+  p.v_cache = V_cache;
+  p.slot_pos = slot_pos;
+  p.block_table = block_table;
+  p.seq_blocks = seq_blocks;
+  p.o = O;
+  p.lse = LSE;
+  p.S = num_seqs;
+  p.Hq = Hq;
+  p.Hkv = Hkv;
+  p.D = D;
+  p.max_blocks = max_blocks;
+  p.block_size = block_size;
+  p.num_blocks = num_blocks;
+  p.scale = softmax_scale;
+  p.ws = workspace;
+  p.stream = (hipStream_t)stream;
+  hipError_t e = kvs::launch_paged_decode(p);
+  return e == hipSuccess ? KVS_OK : hip_fail(e, "paged decode launch");
 }
 
 }  // extern "C"

@@ -153,6 +153,16 @@ __device__ __forceinline__ void dma_b32(const void* base, uint32_t off, uint32_t
       : "v"(off), "s"(base), "s"(lds)
       : "memory");
 }
+// Asynchronous copy of 16 bytes from this lane's own global address to LDS
+// byte address lds + 16 l (gathers whose rows have no common base).
+__device__ __forceinline__ void dma_b128_global(const void* src, uint32_t lds) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(src), "s"(lds)
+      : "memory");
+}
 // A wave-uniform pointer held in scalar registers.
 template <typename T>
 __device__ __forceinline__ const T* uniform_ptr(const T* p) {
@@ -191,6 +201,16 @@ struct Lay {
     return off(8 + 4 * (g16 >> 1) + (li >> 2), 16 * (g16 & 1) + 4 * (li & 3));
   }
 };
+
+// A operand of a 32x32x16 MFMA read transposed from an LDS tile: rows
+// (contraction index) row0 + 4 half + {0..3} and row0 + 8 + 4 half + {0..3}
+// (the order in which the C layout of a score block lists its 16 values),
+// columns c0 + (l % 32).  tl, th = Lay<D>::tr_lo(lane), tr_hi(lane).
+template <int D>
+__device__ __forceinline__ bf16x8 tr_operand(const uint16_t* tile, int row0, int c0, int tl, int th) {
+  const int o = row0 * Lay<D>::PITCH + c0;
+  return cat_tr(lds_read_tr(tile + tl + o), lds_read_tr(tile + th + o));
+}
 
 // Asynchronous global -> LDS copies of an R-row tile (dma_b128:
 // lane l of a wave writes 16 bytes at the wave's LDS base + 16 l, so the 64

@@ -210,16 +210,6 @@ __device__ __forceinline__ void mask_t(f32x16& s, const int* sE, int kb, int j0,
   }
 }
 
-// A operand of a 32x32x16 MFMA read transposed from an LDS tile: rows
-// (contraction index) row0 + 4 half + {0..3} and row0 + 8 + 4 half + {0..3}
-// (the order in which the C layout of a score block lists its 16 values),
-// columns c0 + (l % 32).  tl, th = Lay<D>::tr_lo(lane), tr_hi(lane).
-template <int D>
-__device__ __forceinline__ bf16x8 tr_operand(const uint16_t* tile, int row0, int c0, int tl, int th) {
-  const int o = row0 * Lay<D>::PITCH + c0;
-  return cat_tr(lds_read_tr(tile + tl + o), lds_read_tr(tile + th + o));
-}
-
 // Head grouping of a row-kernel workgroup.
 struct RowTile {
   int g, h, b, i0, i1, i0w, hh;

@@ -48,6 +48,29 @@ hipError_t launch_classify(const int32_t* evict, const int32_t* cu, int B, int T
 hipError_t launch_check(const int32_t* evict, const int32_t* cu, int B, int T, int ntok,
                         int64_t* first_bad, int* cu_bad, hipStream_t stream);
 
+// Paged decode over the streamed KV cache (after host-side validation).
+struct PagedDecode {
+  const void* q;            // [S][Hq][D] bf16
+  const void* k_cache;      // [num_blocks][block_size][Hkv][D] bf16
+  const void* v_cache;
+  const int32_t* slot_pos;  // [num_blocks * block_size]
+  const int32_t* block_table;   // [S][max_blocks]
+  const int32_t* seq_blocks;    // [S]
+  void* o;                  // [S][Hq][D] bf16
+  float* lse;               // [S][Hq]
+  int S, Hq, Hkv, D, max_blocks, block_size, num_blocks;
+  float scale;
+  void* ws;
+  hipStream_t stream;
+};
+int paged_split_slots(int S, int Hkv, int max_blocks, int BS);
+int paged_nsplit(int max_blocks, int BS, int split_slots);
+size_t paged_ws_bytes(int S, int Hq, int D, int nsplit);
+hipError_t launch_paged_append(const void* kn, const void* vn, const int* pos, const int* slots, int n, void* kc,
+                               void* vc, int* slot_pos, int num_slots, int Hkv, int D, hipStream_t stream);
+hipError_t launch_paged_evict(const int* slots, int n, int* slot_pos, int num_slots, hipStream_t stream);
+hipError_t launch_paged_decode(const PagedDecode& p);
+
 // Measured dense bf16 MFMA rate of the current device (TFLOP/s); synchronous.
 hipError_t measure_mfma_rate(double* tflops, hipStream_t stream);
 

@@ -46,6 +46,19 @@ SIGNATURES = {
     "kvs_prof_reset": (None, []),
     "kvs_prof_read": (_I, [ctypes.c_char_p, ctypes.POINTER(_I), ctypes.POINTER(ctypes.c_double)]),
     "kvs_measure_mfma_rate": (_I, [ctypes.POINTER(ctypes.c_double), _P]),
+    # streamed paged KV cache (host block manager: host int32 arrays)
+    "kvs_bm_create": (_I, [_I, _I, _I, _I, ctypes.POINTER(_P)]),
+    "kvs_bm_destroy": (None, [_P]),
+    "kvs_bm_append": (_I, [_P, _I, _P, _I, _P]),
+    "kvs_bm_evict": (_I, [_P, _I, _P, _I, _P]),
+    "kvs_bm_release": (_I, [_P, _I, _P, ctypes.POINTER(_I)]),
+    "kvs_bm_tables": (_I, [_P, _P, _P]),
+    "kvs_bm_free_blocks": (_I, [_P]),
+    "kvs_bm_live": (_I, [_P, _I]),
+    "kvs_paged_append": (_I, [_P, _P, _P, _P, _I, _P, _P, _P, _I, _I, _I, _I, _P]),
+    "kvs_paged_evict": (_I, [_P, _I, _P, _I, _I, _P]),
+    "kvs_paged_decode_workspace": (_Z, [_I, _I, _I, _I, _I, _I]),
+    "kvs_paged_decode": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _F, _P, _Z, _P]),
 }
 for _name, (_res, _args) in SIGNATURES.items():
     _fn = getattr(lib, _name)
@@ -53,7 +66,7 @@ for _name, (_res, _args) in SIGNATURES.items():
     _fn.argtypes = _args
 
 KVS_OK, KVS_ERR_NULL, KVS_ERR_SHAPE, KVS_ERR_ALIGN, KVS_ERR_WORKSPACE, KVS_ERR_EVICT, KVS_ERR_HIP, \
-    KVS_ERR_UNSUPPORTED = range(8)
+    KVS_ERR_UNSUPPORTED, KVS_ERR_CAPACITY, KVS_ERR_STATE = range(10)
 
 
 class KvsError(RuntimeError):

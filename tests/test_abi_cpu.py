@@ -39,8 +39,8 @@ def test_binding_covers_every_symbol(kvs):
 
 
 def test_version_and_strings(kvs):
-    assert kvs.lib.kvs_abi_version() == 1
-    for s in range(8):
+    assert kvs.lib.kvs_abi_version() == 2
+    for s in range(10):
         assert kvs.lib.kvs_status_string(s)
     assert kvs.lib.kvs_status_string(99) == b"unknown status"
 
