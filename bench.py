@@ -135,6 +135,79 @@ def reprefill_compare(wl, kvs, warmup, steps, kvs_ms):
             "time_ratio_reprefill_over_kv_streams": ms / kvs_ms}
 
 
+PEAK_HBM_GBS = 8000.0   # MI355X HBM3E
+
+
+def paged_decode_bench(warmup, steps, S=64, block_size=16):
+    """Decode over the streamed paged KV cache (the inference side): S rollouts
+    shaped like the 16k keep-all trace (Hq=32, Hkv=8, D=128, 16-token blocks)
+    are streamed through one cache segment by segment (turns and summary
+    appended, then the turns evicted, freed blocks reused across rollouts),
+    and one query per rollout is decoded at the last token.  HBM-bound: the
+    algorithmic bytes are the live K and V entries read once (plus Q and O)."""
+    import torch
+
+    from paper_2609_35750_amd import inputs, paged
+    from paper_2609_35750_amd import kvs
+
+    L, p, w, s_, Hq, Hkv, D = 16384, 1024, 4096, 512, 32, 8, 128
+    e = inputs.evict_at_layout(L, p, w, s_, "keep_all")
+    dev = torch.device("cuda:0")
+    max_blocks = (L + block_size - 1) // block_size + 1
+    live_max = int(np.sum(np.minimum(e, L) > L - 1))
+    nb = S * ((live_max + w + s_) // block_size + 4)
+    cache = paged.PagedKVCache(nb, block_size, S, max_blocks, Hkv, D, device=dev)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(1234)
+    # eviction events: positions evicted at each time
+    ev_t = {}
+    for j, x in enumerate(np.minimum(e, L)):
+        if x < L:
+            ev_t.setdefault(int(x), []).append(j)
+    cuts = sorted(set(ev_t) | {L})
+    for sq in range(S):
+        t0 = 0
+        for t1 in cuts:
+            if t0 < t1:
+                n = t1 - t0
+                kn = torch.randn((n, Hkv, D), generator=gen, device=dev).to(torch.bfloat16)
+                vn = torch.randn((n, Hkv, D), generator=gen, device=dev).to(torch.bfloat16)
+                cache.append(sq, np.arange(t0, t1), kn, vn)
+            if t1 < L:
+                cache.evict(sq, ev_t[t1])
+            t0 = t1
+    live = sum(cache.bm.live(sq) for sq in range(S))
+    q = torch.randn((S, Hq, D), generator=gen, device=dev).to(torch.bfloat16)
+    o = torch.empty_like(q)
+    lse = torch.empty((S, Hq), dtype=torch.float32, device=dev)
+    for _ in range(warmup):
+        cache.decode(q, 1.0 / math.sqrt(D), out=o, lse=lse)
+    torch.cuda.synchronize()
+    kvs.kvs_prof_reset()
+    kvs.kvs_prof_enable(True)
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        cache.decode(q, 1.0 / math.sqrt(D), out=o, lse=lse)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    kvs.kvs_prof_enable(False)
+    n, ms = kvs.kvs_prof_read("paged_decode")
+    kvs.kvs_prof_reset()
+    kern_ms = ms / max(n, 1)
+    kv_bytes = live * Hkv * D * 2 * 2
+    io_bytes = 2 * S * Hq * D * 2 + S * Hq * 4
+    algo = kv_bytes + io_bytes
+    achieved = algo / (kern_ms * 1e-3) / 1e9
+    return {
+        "workload": f"{S} rollouts of the 16k keep-all trace (Hq={Hq}, Hkv={Hkv}, D={D}) decoded at token {L - 1}",
+        "block_size": block_size, "live_entries": live, "cache_blocks": nb,
+        "call_ms": (t1 - t0) * 1e3 / steps, "kernel_ms": kern_ms,
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": achieved / PEAK_HBM_GBS, "traffic": None, "kernel": "paged_decode",
+                     "algorithmic_bytes_per_launch": algo},
+    }
+
+
 def cpu_baseline(wl, tensors, evict_at, heads=2):
     """The fp64 checker as it stands, timed on q-heads [0, heads) of KV head 0."""
     from oracle import attention as orc
@@ -168,6 +241,7 @@ def main():
     ap.add_argument("--workload", default="trace16k_gqa4")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU checker timing")
     ap.add_argument("--no-reprefill", action="store_true", help="skip the re-prefill comparison")
+    ap.add_argument("--no-decode", action="store_true", help="skip the paged-cache decode measurement")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (see DESIGN.md for how it would "
@@ -264,6 +338,8 @@ def main():
     roofline["frac_of_measured_peak"] = achieved / measured_peak
     if not args.no_reprefill:
         out["reprefill"] = reprefill_compare(wl, kvs, args.warmup, args.steps, ms_per_step)
+    if not args.no_decode:
+        out["paged_decode"] = paged_decode_bench(args.warmup, args.steps)
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(wl, tensors, e)
     print(json.dumps(out), flush=True)

@@ -183,7 +183,8 @@ kvs_status_t kvs_measure_mfma_rate(double* tflops, void* stream);
  * padded to 16 tokens) or 1 (the SGLang setup); any size in [1, 64] works.
  *
  * Device cache (caller-owned, allocated once):
- *   K_cache, V_cache  bf16 [num_blocks][block_size][Hkv][D]  (16-byte aligned)
+ *   K_cache, V_cache  bf16 [num_blocks][Hkv][block_size][D]  (16-byte aligned; a
+ *                     block holds one contiguous run of block_size rows per KV head)
  *   slot_pos          int32 [num_blocks * block_size]: trace position of the
  *                     token held by each slot, -1 for an empty or evicted slot.
  *                     Must be filled with -1 before first use.
@@ -235,7 +236,7 @@ int kvs_bm_live(const kvs_block_manager* bm, int seq);
 /* ---- device updates (enqueued on `stream`) */
 
 /* Write n new tokens into the cache: K_new, V_new bf16 [n][Hkv][D] go to
- * slots[0..n) of K_cache, V_cache and slot_pos[slots[t]] = positions[t]
+ * slots[0..n) of K_cache, V_cache and slot_pos[slots[t]] = positions[t] (slot = block * block_size + row)
  * (positions, slots: device int32 [n]).  Slots outside [0, num_blocks *
  * block_size) are skipped (the device cannot report them). */
 kvs_status_t kvs_paged_append(const void* K_new, const void* V_new, const int32_t* positions,

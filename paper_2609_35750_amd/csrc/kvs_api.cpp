@@ -436,7 +436,7 @@ kvs_status_t kvs_paged_append(const void* K_new, const void* V_new, const int32_
   REQUIRE_PTR(V_new, "V_new");
   if (!positions || !slots) return fail(KVS_ERR_NULL, "positions or slots is NULL");
   hipError_t e = kvs::launch_paged_append(K_new, V_new, positions, slots, n, K_cache, V_cache, slot_pos,
-                                          num_blocks * block_size, Hkv, D, (hipStream_t)stream);
+                                          num_blocks * block_size, block_size, Hkv, D, (hipStream_t)stream);
   return e == hipSuccess ? KVS_OK : hip_fail(e, "paged append launch");
 }
 
@@ -462,16 +462,14 @@ static kvs_status_t check_decode_dims(int S, int Hq, int Hkv, int D, int num_blo
   if (Hq / Hkv > 32) return fail(KVS_ERR_UNSUPPORTED, "decode supports GQA groups of at most 32 (got %d)", Hq / Hkv);
   if ((long long)max_blocks * block_size > 0x7fffffffll)
     return fail(KVS_ERR_UNSUPPORTED, "max_blocks * block_size above INT32_MAX");
-  if ((long long)S * Hkv * kvs::paged_nsplit(max_blocks, block_size, kvs::paged_split_slots(S, Hkv, max_blocks, block_size)) >
-      0x7fffffffll)
+  if ((long long)S * Hkv * kvs::paged_nsplit(S, Hkv, max_blocks, block_size, D) > 0x7fffffffll)
     return fail(KVS_ERR_UNSUPPORTED, "decode grid too large");
   return KVS_OK;
 }
 
 size_t kvs_paged_decode_workspace(int num_seqs, int Hq, int Hkv, int D, int max_blocks, int block_size) {
   if (num_seqs < 1 || Hkv < 1 || max_blocks < 1 || block_size < 1) return 0;
-  const int per = kvs::paged_split_slots(num_seqs, Hkv, max_blocks, block_size);
-  return kvs::paged_ws_bytes(num_seqs, Hq, D, kvs::paged_nsplit(max_blocks, block_size, per));
+  return kvs::paged_ws_bytes(num_seqs, Hq, D, kvs::paged_nsplit(num_seqs, Hkv, max_blocks, block_size, D));
 }
 
 kvs_status_t kvs_paged_decode(const void* Q, const void* K_cache, const void* V_cache, const int32_t* slot_pos,

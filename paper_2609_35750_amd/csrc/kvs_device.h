@@ -163,6 +163,16 @@ __device__ __forceinline__ void dma_b128_global(const void* src, uint32_t lds) {
       : "v"(src), "s"(lds)
       : "memory");
 }
+// Asynchronous copy of 4 bytes from this lane's own global address to LDS byte
+// address lds + 4 l.
+__device__ __forceinline__ void dma_b32_global(const void* src, uint32_t lds) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %1, off\n\ts_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(src), "s"(lds)
+      : "memory");
+}
 // A wave-uniform pointer held in scalar registers.
 template <typename T>
 __device__ __forceinline__ const T* uniform_ptr(const T* p) {

@@ -51,7 +51,7 @@ hipError_t launch_check(const int32_t* evict, const int32_t* cu, int B, int T, i
 // Paged decode over the streamed KV cache (after host-side validation).
 struct PagedDecode {
   const void* q;            // [S][Hq][D] bf16
-  const void* k_cache;      // [num_blocks][block_size][Hkv][D] bf16
+  const void* k_cache;      // [num_blocks][Hkv][block_size][D] bf16
   const void* v_cache;
   const int32_t* slot_pos;  // [num_blocks * block_size]
   const int32_t* block_table;   // [S][max_blocks]
@@ -63,11 +63,10 @@ struct PagedDecode {
   void* ws;
   hipStream_t stream;
 };
-int paged_split_slots(int S, int Hkv, int max_blocks, int BS);
-int paged_nsplit(int max_blocks, int BS, int split_slots);
+int paged_nsplit(int S, int Hkv, int max_blocks, int BS, int D);
 size_t paged_ws_bytes(int S, int Hq, int D, int nsplit);
 hipError_t launch_paged_append(const void* kn, const void* vn, const int* pos, const int* slots, int n, void* kc,
-                               void* vc, int* slot_pos, int num_slots, int Hkv, int D, hipStream_t stream);
+                               void* vc, int* slot_pos, int num_slots, int BS, int Hkv, int D, hipStream_t stream);
 hipError_t launch_paged_evict(const int* slots, int n, int* slot_pos, int num_slots, hipStream_t stream);
 hipError_t launch_paged_decode(const PagedDecode& p);
 

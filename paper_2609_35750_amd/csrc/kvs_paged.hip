@@ -4,10 +4,11 @@
 // to a paged cache and drops evicted entries for good; a query attends over
 // exactly the entries that are live when it is generated.
 //
-// Cache layout: K, V [num_blocks][block_size][Hkv][D] bf16; slot_pos
-// [num_blocks * block_size] int32 holds the trace position of the token in a
-// slot, or -1 (empty or evicted).  A sequence's blocks are listed in its row of
-// the block table.
+// Cache layout: K, V [num_blocks][Hkv][block_size][D] bf16 (a block holds one
+// contiguous run of block_size rows per KV head); slot_pos [num_blocks *
+// block_size] int32 holds the trace position of the token in a slot (slot =
+// block * block_size + row), or -1 (empty or evicted).  A sequence's blocks are
+// listed in its row of the block table.
 //
 // Decode: one wave per (sequence, KV head, split).  The wave walks its split's
 // cache slots in tiles of 32, gathering each tile's K and V rows from their
@@ -20,6 +21,8 @@
 #include "kvs_device.h"
 #include "kvs_launch.h"
 
+#include <algorithm>
+
 namespace kvs {
 
 // ---------------------------------------------------------------- append / evict
@@ -29,7 +32,7 @@ __global__ void __launch_bounds__(256) paged_append_kernel(const uint16_t* __res
                                                            const uint16_t* __restrict__ vn,
                                                            const int* __restrict__ pos, const int* __restrict__ slots,
                                                            int n, uint16_t* __restrict__ kc, uint16_t* __restrict__ vc,
-                                                           int* __restrict__ slot_pos, int num_slots, int Hkv) {
+                                                           int* __restrict__ slot_pos, int num_slots, int Hkv, int BS) {
   const long long per_tok = (long long)Hkv * (D / 8);   // 16-byte chunks per token and tensor
   const long long chunks = (long long)n * per_tok;
   for (long long c = (long long)blockIdx.x * blockDim.x + threadIdx.x; c < chunks;
@@ -37,7 +40,8 @@ __global__ void __launch_bounds__(256) paged_append_kernel(const uint16_t* __res
     const long long t = c / per_tok, r = c - t * per_tok;
     const int slot = slots[t];
     if ((unsigned)slot >= (unsigned)num_slots) continue;
-    const long long dst = ((long long)slot * per_tok + r) * 8;
+    const int h = (int)(r / (D / 8)), d8 = (int)(r - (long long)h * (D / 8));
+    const long long dst = ((((long long)(slot / BS) * Hkv + h) * BS + slot % BS) * D) + 8 * d8;
     *reinterpret_cast<uint4*>(kc + dst) = *reinterpret_cast<const uint4*>(kn + c * 8);
     *reinterpret_cast<uint4*>(vc + dst) = *reinterpret_cast<const uint4*>(vn + c * 8);
     if (r == 0) slot_pos[slot] = pos[t];
@@ -62,7 +66,7 @@ struct DecodeArgs {
   const int* nblk;        // [S]
   float* part;            // [S][Hq][nsplit][D]: unnormalised O of each split (relative to its max)
   float* part_ml;         // [S][Hq][nsplit][2]: max (log2 units), sum
-  int S, Hq, Hkv, G, max_blocks, BS, num_blocks, nsplit, split_slots;
+  int S, Hq, Hkv, G, max_blocks, BS, num_blocks, nsplit;
   float scale_log2;       // softmax_scale * log2(e)
 };
 
@@ -86,30 +90,63 @@ struct GatherStager {
       col[i] = (q < SLOTS && pc < LY::CPR) ? 8 * (pc ^ LY::flip(r)) : 0;
     }
   }
-  // rslot: cache slot of tile row (lane % 32) in lanes 0..31 (any valid slot);
-  // src: cache base with the KV head offset applied; tok_stride: elements per cache slot.
-  __device__ __forceinline__ void issue(uint32_t lds, const uint16_t* __restrict__ src, long long tok_stride,
-                                        int rslot) const {
-    const uint16_t* base = uniform_ptr(src);
+  // K and V rows of one tile.  roff: element offset of tile row (lane % 32)
+  // in the caches (lanes 0..31, a valid row).  The offsets of all pieces are
+  // exchanged first (one LDS round trip), then the copies are issued back to back.
+  __device__ __forceinline__ void issue(uint32_t ldsK, uint32_t ldsV, const uint16_t* __restrict__ kb,
+                                        const uint16_t* __restrict__ vb, long long roff) const {
+    int lo[NI], hi[NI];
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
       const int r = row[i] < 0 ? 0 : row[i];
-      const int slot = max(__shfl(rslot, r), 0);   // invalid slots (< 0) read slot 0 (masked)
+      lo[i] = __shfl((int)(uint32_t)roff, r);
+      hi[i] = __shfl((int)(roff >> 32), r);
+    }
+    __builtin_amdgcn_sched_barrier(0);   // all exchanges before the first copy
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
       if (i * kWave + kWave <= SLOTS || row[i] >= 0) {
-        const long long off = (long long)slot * tok_stride + col[i];
-        dma_b128_global(base + off, lds + i * kWave * 16);
+        const long long off = (long long)(((uint64_t)(uint32_t)hi[i] << 32) | (uint32_t)lo[i]) + col[i];
+        dma_b128_global(kb + off, ldsK + i * kWave * 16);
+        dma_b128_global(vb + off, ldsV + i * kWave * 16);
       }
     }
   }
 };
 
+// Copies in flight per wave: a ring of kDecRing tiles (K, V and the tile's
+// slot_pos values), one ahead of the one being computed.  D = 128 uses 37 KB
+// of LDS per wave, so four waves (one per SIMD) share a CU; D = 64 18 KB
+// (eight).  A deeper ring costs SIMDs: four stages at two waves per CU
+// measured 20% slower on the 64-rollout decode.
+constexpr int kDecRing = 2;
+
+// Wait until at most N vector memory operations of this wave are outstanding (N <= 63).
+template <int N>
+__device__ __forceinline__ void wait_vm_le() {
+  static_assert(N >= 0 && N < 64, "vmcnt is six bits");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
+}
+
+// Every global read of the decode loop is an asynchronous copy to LDS, so all
+// of them complete in issue order under one counter and each wait is exact
+// (R = kDecRing):
+// step n reads the block-table entries of tile n + R - 1 (copied during step
+// n - 1), issues the table copy of tile n + R, the K/V copy of tile n + R - 1
+// and the copy of its slot_pos values, and computes tile n once at most the
+// copies of the R - 1 later steps are outstanding.  (A compiler-visible load
+// consumed while copies are in flight would make the compiler wait for all
+// of them, since it cannot see them.)
 template <int D>
 __global__ void __launch_bounds__(64) paged_decode_kernel(DecodeArgs a) {
-  constexpr int KS = D / 16, DB = D / 32, PITCH = Lay<D>::PITCH;
-  __shared__ __attribute__((aligned(1024))) uint16_t sK0[kDecTile * PITCH];
-  __shared__ __attribute__((aligned(1024))) uint16_t sK1[kDecTile * PITCH];
-  __shared__ __attribute__((aligned(1024))) uint16_t sV0[kDecTile * PITCH];
-  __shared__ __attribute__((aligned(1024))) uint16_t sV1[kDecTile * PITCH];
+  constexpr int KS = D / 16, DB = D / 32, PITCH = Lay<D>::PITCH, TILE = kDecTile * PITCH, R = kDecRing;
+  constexpr int OPS_KV = 2 * GatherStager<D>::NI;   // K and V copy instructions per tile
+  constexpr int OPS_STEP = OPS_KV + 2;             // plus the table and slot_pos copies
+  static_assert((R - 1) * OPS_STEP < 64, "outstanding copies must fit vmcnt");
+  __shared__ __attribute__((aligned(1024))) uint16_t sK[R * TILE];
+  __shared__ __attribute__((aligned(1024))) uint16_t sV[R * TILE];
+  __shared__ __attribute__((aligned(256))) int sTab[2][kWave];   // block-table entries of a tile's rows
+  __shared__ __attribute__((aligned(256))) int sPos[R][kWave];   // slot_pos of a tile's rows
 
   int wg = blockIdx.x;
   const int sp = wg % a.nsplit;
@@ -121,8 +158,10 @@ __global__ void __launch_bounds__(64) paged_decode_kernel(DecodeArgs a) {
 
   // blocks in use by sequence s (clamped to the table width; some slots may be evicted)
   const int nslots = min(max(a.nblk[s], 0), a.max_blocks) * a.BS;
-  const int c_begin = sp * a.split_slots;
-  const int c_end = min(c_begin + a.split_slots, nslots);
+  // the sequence's slots in nsplit equal ranges of whole tiles
+  const int per = ((nslots + a.nsplit - 1) / a.nsplit + kDecTile - 1) / kDecTile * kDecTile;
+  const int c_begin = min(sp * per, nslots);
+  const int c_end = min(c_begin + per, nslots);
   const int ntile = c_end > c_begin ? (c_end - c_begin + kDecTile - 1) / kDecTile : 0;
 
   // Q^T operand: column n = q-head g * G + n of the group (zero for n >= G)
@@ -143,96 +182,90 @@ __global__ void __launch_bounds__(64) paged_decode_kernel(DecodeArgs a) {
   float m_run = -INFINITY, l_run = 0.f;
 
   const int* trow = a.table + (size_t)s * a.max_blocks;
-  const long long tok_stride = (long long)a.Hkv * D;
-  const uint16_t* kbase = a.kc + (long long)g * D;
-  const uint16_t* vbase = a.vc + (long long)g * D;
+  const long long blk_stride = (long long)a.Hkv * a.BS * D;   // elements per cache block
+  const uint16_t* kbase = a.kc + (long long)g * a.BS * D;
+  const uint16_t* vbase = a.vc + (long long)g * a.BS * D;
   GatherStager<D> gst;
   gst.init(lane);
 
-  // Slot of tile row `col` of tile t (lanes 0..31 meaningful; rows past c_end
-  // repeat the tile's first slot and are masked).
-  auto slot_of = [&](int t) __attribute__((always_inline)) {
-    const int c0 = c_begin + t * kDecTile;
-    const int c = min(c0 + col, c_end - 1);
-    const int blk = trow[c / a.BS];
-    // a table entry outside the cache reads slot 0 and is masked by live_of
-    return (unsigned)blk < (unsigned)a.num_blocks ? blk * a.BS + c % a.BS : -1 - (c % a.BS);
-  };
-  // Live mask of tile t: bit r set iff row r is a live slot of the sequence.
-  auto live_of = [&](int t, int slot) __attribute__((always_inline)) {
-    const int c = c_begin + t * kDecTile + col;
-    const bool ok = lane < 32 && c < c_end && slot >= 0 && a.slot_pos[slot] >= 0;
-    return (unsigned)__ballot(ok);
+  // sequence-local slot index of tile row `col` of tile t (rows past c_end
+  // repeat the split's last slot and are masked)
+  auto slot_index = [&](int t) __attribute__((always_inline)) { return min(c_begin + t * kDecTile + col, c_end - 1); };
+  // copy the block-table entries of tile t's rows (lanes 0..31) into sTab[t & 1]
+  auto copy_table = [&](int t) __attribute__((always_inline)) {
+    const int c = slot_index(t);
+    if (lane < 32) dma_b32_global(trow + c / a.BS, lds_addr(&sTab[t & 1][0]));
   };
 
-  int slot_cur = 0, slot_nxt = 0;
-  unsigned live_cur = 0u;
-  if (ntile > 0) {
-    slot_cur = slot_of(0);
-    live_cur = live_of(0, slot_cur);
-    gst.issue(lds_addr(sK0), kbase, tok_stride, slot_cur);
-    gst.issue(lds_addr(sV0), vbase, tok_stride, slot_cur);
-    if (ntile > 1) slot_nxt = slot_of(1);
-  }
-  wait_vm();
-
-  auto body = [&](int t, const uint16_t* cK, const uint16_t* cV, uint16_t* nK, uint16_t* nV)
-      __attribute__((always_inline)) {
-    unsigned live_nxt = 0u;
-    int slot_nn = 0;
-    if (t + 1 < ntile) {
-      gst.issue(lds_addr(nK), kbase, tok_stride, slot_nxt);
-      gst.issue(lds_addr(nV), vbase, tok_stride, slot_nxt);
-      live_nxt = live_of(t + 1, slot_nxt);
-      if (t + 2 < ntile) slot_nn = slot_of(t + 2);
+  unsigned valid_q[R] = {};   // rows of tiles n .. n + R - 1 that hold a slot of the split (index 0 = tile n)
+  if (ntile > 0) copy_table(0);
+  wait_vm_le<0>();   // Q and the first table entries are in (no compiler-visible load stays pending in the loop)
+  for (int n = -(R - 1); n < ntile; ++n) {
+    const int tn = n + R - 1;   // tile whose copies this step issues
+    if (tn < ntile) {
+      if (n > -(R - 1)) wait_vm_le<OPS_KV + 1>();   // table entries of tile tn have landed
+      const int c = slot_index(tn);
+      const int blk = sTab[tn & 1][col];
+      // a table entry outside the cache reads slot 0 and is masked
+      const bool bok = (unsigned)blk < (unsigned)a.num_blocks;
+      const int slot = bok ? blk * a.BS + c % a.BS : 0;
+      const long long roff = bok ? (long long)blk * blk_stride + (long long)(c % a.BS) * D : 0;
+      copy_table(min(tn + 1, ntile - 1));   // always one copy, so that every step issues the same count
+      gst.issue(lds_addr(sK + (tn % R) * TILE), lds_addr(sV + (tn % R) * TILE), kbase, vbase, roff);
+      if (lane < 32) dma_b32_global(a.slot_pos + slot, lds_addr(&sPos[tn % R][0]));
+      valid_q[R - 1] = (unsigned)__ballot(lane < 32 && c_begin + tn * kDecTile + col < c_end && bok);
+      if (n >= 0) wait_vm_le<(R - 1) * OPS_STEP>();   // tile n has landed
+    } else if (n >= 0) {
+      wait_vm_le<0>();
     }
-    if (live_cur != 0u) {
-      // S^T block: keys on M (tile rows), q-heads on N
-      f32x16 sc = f32x16{};
-      bf16x8 ka[KS];
+    if (n >= 0) {
+      const unsigned live_cur = valid_q[0] & (unsigned)__ballot(lane < 32 && sPos[n % R][col] >= 0);
+      const uint16_t* cK = sK + (n % R) * TILE;
+      const uint16_t* cV = sV + (n % R) * TILE;
+      if (live_cur != 0u) {
+        // S^T block: keys on M (tile rows), q-heads on N
+        f32x16 sc = f32x16{};
+        bf16x8 ka[KS];
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) ka[ks] = lds_read_b128(cK + rl + 16 * ks);
+        for (int ks = 0; ks < KS; ++ks) ka[ks] = lds_read_b128(cK + rl + 16 * ks);
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) sc = mfma32(ka[ks], qreg[ks], sc);
-      // element r <-> tile row 8 (r / 4) + 4 half + r % 4
+        for (int ks = 0; ks < KS; ++ks) sc = mfma32(ka[ks], qreg[ks], sc);
+        // element r <-> tile row 8 (r / 4) + 4 half + r % 4
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = 8 * (r >> 2) + 4 * half + (r & 3);
-        if (!((live_cur >> row) & 1u)) sc[r] = -INFINITY;
-      }
-      float mx = -INFINITY;
+        for (int r = 0; r < 16; ++r) {
+          const int row = 8 * (r >> 2) + 4 * half + (r & 3);
+          if (!((live_cur >> row) & 1u)) sc[r] = -INFINITY;
+        }
+        float mx = -INFINITY;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[r]);
-      mx = halves_max(mx) * a.scale_log2;
-      if (mx > m_run) {   // per column (lane); no divergence cost worth avoiding here
-        const float alpha = __builtin_amdgcn_exp2f(m_run - mx);   // 0 on the first live tile
-        l_run *= alpha;
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[r]);
+        mx = halves_max(mx) * a.scale_log2;
+        if (mx > m_run) {   // per column (lane)
+          const float alpha = __builtin_amdgcn_exp2f(m_run - mx);   // 0 on the first live tile
+          l_run *= alpha;
 #pragma unroll
-        for (int d = 0; d < DB; ++d)
+          for (int d = 0; d < DB; ++d)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) acc[d][r] *= alpha;
-        m_run = mx;
-      }
-      const float m_use = m_run == -INFINITY ? 0.f : m_run;
+            for (int r = 0; r < 16; ++r) acc[d][r] *= alpha;
+          m_run = mx;
+        }
+        const float m_use = m_run == -INFINITY ? 0.f : m_run;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        sc[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[r], a.scale_log2, -m_use));
-        l_run += sc[r];
-      }
+        for (int r = 0; r < 16; ++r) {
+          sc[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[r], a.scale_log2, -m_use));
+          l_run += sc[r];
+        }
 #pragma unroll
-      for (int t2 = 0; t2 < 2; ++t2) {
-        const bf16x8 pb = pack8(sc, 8 * t2);
+        for (int t2 = 0; t2 < 2; ++t2) {
+          const bf16x8 pb = pack8(sc, 8 * t2);
 #pragma unroll
-        for (int d = 0; d < DB; ++d) acc[d] = mfma32(tr_operand<D>(cV, 16 * t2, 32 * d, tl, th), pb, acc[d]);
+          for (int d = 0; d < DB; ++d) acc[d] = mfma32(tr_operand<D>(cV, 16 * t2, 32 * d, tl, th), pb, acc[d]);
+        }
       }
     }
-    wait_vm();   // tile t + 1 has landed in this wave's buffers
-    live_cur = live_nxt;
-    slot_nxt = slot_nn;
-  };
-  for (int t = 0; t < ntile; t += 2) {
-    body(t, sK0, sV0, sK1, sV1);
-    if (t + 1 < ntile) body(t + 1, sK1, sV1, sK0, sV0);
+#pragma unroll
+    for (int i = 0; i < R - 1; ++i) valid_q[i] = valid_q[i + 1];
+    valid_q[R - 1] = 0u;
   }
 
   // partial of this split for q-head column `col`
@@ -240,12 +273,14 @@ __global__ void __launch_bounds__(64) paged_decode_kernel(DecodeArgs a) {
   if (col_ok) {
     const size_t pidx = ((size_t)s * a.Hq + hcol) * a.nsplit + sp;
     float* dst = a.part + pidx * D;
+    if (l_tot > 0.f) {   // an empty split leaves its O unwritten (the merge skips it)
 #pragma unroll
-    for (int d = 0; d < DB; ++d)
+      for (int d = 0; d < DB; ++d)
 #pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4)
-        *reinterpret_cast<float4*>(dst + 32 * d + 8 * q4 + 4 * half) =
-            make_float4(acc[d][4 * q4], acc[d][4 * q4 + 1], acc[d][4 * q4 + 2], acc[d][4 * q4 + 3]);
+        for (int q4 = 0; q4 < 4; ++q4)
+          *reinterpret_cast<float4*>(dst + 32 * d + 8 * q4 + 4 * half) =
+              make_float4(acc[d][4 * q4], acc[d][4 * q4 + 1], acc[d][4 * q4 + 2], acc[d][4 * q4 + 3]);
+    }
     if (half == 0) {
       a.part_ml[2 * pidx] = m_run;
       a.part_ml[2 * pidx + 1] = l_tot;
@@ -286,31 +321,25 @@ __global__ void __launch_bounds__(256) paged_combine_kernel(const float* __restr
 }
 
 template __global__ void paged_append_kernel<64>(const uint16_t*, const uint16_t*, const int*, const int*, int,
-                                                 uint16_t*, uint16_t*, int*, int, int);
+                                                 uint16_t*, uint16_t*, int*, int, int, int);
 template __global__ void paged_append_kernel<128>(const uint16_t*, const uint16_t*, const int*, const int*, int,
-                                                  uint16_t*, uint16_t*, int*, int, int);
+                                                  uint16_t*, uint16_t*, int*, int, int, int);
 template __global__ void paged_decode_kernel<64>(DecodeArgs);
 template __global__ void paged_decode_kernel<128>(DecodeArgs);
 template __global__ void paged_combine_kernel<64>(const float*, const float*, int, int, uint16_t*, float*);
 template __global__ void paged_combine_kernel<128>(const float*, const float*, int, int, uint16_t*, float*);
 
 // ---------------------------------------------------------------- launchers
-// Slots per split: a multiple of the tile, chosen so that the grid holds at
-// least ~4 waves per CU when the sequences are long enough.
-int paged_split_slots(int S, int Hkv, int max_blocks, int BS) {
+// Key splits per (sequence, KV head): enough waves for one round of the
+// resident ones (D = 128: four per CU, D = 64: eight; each sequence's live
+// slots are cut into that many equal ranges on the device), at most one split
+// per four tiles of the table width.
+int paged_nsplit(int S, int Hkv, int max_blocks, int BS, int D) {
   const long long max_slots = (long long)max_blocks * BS;
-  const long long want_waves = 4ll * 256;
   const long long units = (long long)S * Hkv;
-  long long splits = (want_waves + units - 1) / units;
-  if (splits < 1) splits = 1;
-  long long per = (max_slots + splits - 1) / splits;
-  per = ((per + 255) / 256) * 256;   // at least 8 tiles per split
-  if (per < 256) per = 256;
-  return (int)per;
-}
-int paged_nsplit(int max_blocks, int BS, int split_slots) {
-  const long long max_slots = (long long)max_blocks * BS;
-  return (int)((max_slots + split_slots - 1) / split_slots);
+  long long splits = ((D == 128 ? 4ll : 8ll) * 256 + units - 1) / units;
+  splits = std::min(splits, std::max(1ll, max_slots / (4 * kDecTile)));
+  return (int)std::max(1ll, splits);
 }
 size_t paged_ws_bytes(int S, int Hq, int D, int nsplit) {
   const size_t rows = (size_t)S * Hq * nsplit;
@@ -318,16 +347,16 @@ size_t paged_ws_bytes(int S, int Hq, int D, int nsplit) {
 }
 
 hipError_t launch_paged_append(const void* kn, const void* vn, const int* pos, const int* slots, int n, void* kc,
-                               void* vc, int* slot_pos, int num_slots, int Hkv, int D, hipStream_t stream) {
+                               void* vc, int* slot_pos, int num_slots, int BS, int Hkv, int D, hipStream_t stream) {
   if (n == 0) return hipSuccess;
   const long long chunks = (long long)n * Hkv * (D / 8);
   const int blocks = (int)std::min<long long>((chunks + 255) / 256, 65535);
   if (D == 128)
     hipLaunchKernelGGL(paged_append_kernel<128>, dim3(blocks), dim3(256), 0, stream, (const uint16_t*)kn,
-                       (const uint16_t*)vn, pos, slots, n, (uint16_t*)kc, (uint16_t*)vc, slot_pos, num_slots, Hkv);
+                       (const uint16_t*)vn, pos, slots, n, (uint16_t*)kc, (uint16_t*)vc, slot_pos, num_slots, Hkv, BS);
   else
     hipLaunchKernelGGL(paged_append_kernel<64>, dim3(blocks), dim3(256), 0, stream, (const uint16_t*)kn,
-                       (const uint16_t*)vn, pos, slots, n, (uint16_t*)kc, (uint16_t*)vc, slot_pos, num_slots, Hkv);
+                       (const uint16_t*)vn, pos, slots, n, (uint16_t*)kc, (uint16_t*)vc, slot_pos, num_slots, Hkv, BS);
   return hipGetLastError();
 }
 
@@ -353,8 +382,7 @@ hipError_t launch_paged_decode(const PagedDecode& p) {
   a.max_blocks = p.max_blocks;
   a.BS = p.block_size;
   a.num_blocks = p.num_blocks;
-  a.split_slots = paged_split_slots(p.S, p.Hkv, p.max_blocks, p.block_size);
-  a.nsplit = paged_nsplit(p.max_blocks, p.block_size, a.split_slots);
+  a.nsplit = paged_nsplit(p.S, p.Hkv, p.max_blocks, p.block_size, p.D);
   a.part = (float*)p.ws;
   const size_t rows = (size_t)p.S * p.Hq * a.nsplit;
   a.part_ml = (float*)((char*)p.ws + ((rows * p.D * sizeof(float) + 255) & ~(size_t)255));

@@ -90,9 +90,9 @@ def kvs_paged_evict(slots, slot_pos, num_blocks: int, block_size: int) -> None:
 
 def kvs_paged_decode(q, k_cache, v_cache, slot_pos, block_table, seq_blocks, softmax_scale=None,
                      out=None, lse=None) -> Tuple[torch.Tensor, torch.Tensor]:
-    """``kvs_paged_decode``: q [S, Hq, D] bf16; caches [num_blocks, block_size, Hkv, D]; returns (O, LSE)."""
+    """``kvs_paged_decode``: q [S, Hq, D] bf16; caches [num_blocks, Hkv, block_size, D]; returns (O, LSE)."""
     S, Hq, D = q.shape
-    nb, bs, Hkv, Dk = k_cache.shape
+    nb, Hkv, bs, Dk = k_cache.shape
     if Dk != D or v_cache.shape != k_cache.shape:
         raise ValueError("cache shapes do not match q")
     if q.dtype != torch.bfloat16 or k_cache.dtype != torch.bfloat16 or v_cache.dtype != torch.bfloat16:
@@ -130,7 +130,7 @@ class PagedKVCache:
         self.num_blocks, self.block_size, self.num_seqs, self.max_blocks = num_blocks, block_size, num_seqs, max_blocks
         self.Hkv, self.D = Hkv, D
         self.device = torch.device(device)
-        self.k = torch.zeros((num_blocks, block_size, Hkv, D), dtype=torch.bfloat16, device=self.device)
+        self.k = torch.zeros((num_blocks, Hkv, block_size, D), dtype=torch.bfloat16, device=self.device)
         self.v = torch.zeros_like(self.k)
         self.slot_pos = torch.full((num_blocks * block_size,), -1, dtype=torch.int32, device=self.device)
         self._tables = None

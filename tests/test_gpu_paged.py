@@ -122,7 +122,8 @@ def test_decode_over_streamed_cache_matches_masked_rows(pg, case):
     # cache contents: live slots hold exactly R(L-1), with the appended K/V bits
     slot_pos = cache.slot_pos.cpu().numpy()
     table, nblk = cache.bm.tables()
-    kc = cache.k.cpu().view(torch.int16).numpy().reshape(-1, Hkv, D)
+    # [block][Hkv][row][D] -> per slot [slot][Hkv][D]
+    kc = cache.k.cpu().view(torch.int16).numpy().transpose(0, 2, 1, 3).reshape(-1, Hkv, D)
     for i, sq in enumerate(seqs):
         slots = np.concatenate([np.arange(b * bs, (b + 1) * bs) for b in table[i, : nblk[i]]]) if nblk[i] else []
         pos = slot_pos[slots]
