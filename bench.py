@@ -203,8 +203,8 @@ def paged_decode_bench(warmup, steps, S=64, block_size=16):
         "block_size": block_size, "live_entries": live, "cache_blocks": nb,
         "call_ms": (t1 - t0) * 1e3 / steps, "kernel_ms": kern_ms,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                     "frac": achieved / PEAK_HBM_GBS, "traffic": None, "kernel": "paged_decode",
-                     "algorithmic_bytes_per_launch": algo},
+                     "frac": achieved / PEAK_HBM_GBS, "traffic": load_traffic("paged_decode", "trace16k_gqa4"),
+                     "kernel": "paged_decode", "algorithmic_bytes_per_launch": algo},
     }
 
 

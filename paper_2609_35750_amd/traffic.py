@@ -27,12 +27,12 @@ from collections import defaultdict
 
 COPY_BYTES = 1 << 30
 KERNELS = {"fwd_kernel": "fwd", "dkdv_kernel": "bwd_dkdv", "dq_kernel": "bwd_dq", "bwd_pre_kernel": "bwd_pre",
-           "kstats_kernel": "classify"}
+           "kstats_kernel": "classify", "paged_decode_kernel": "paged_decode"}
 
 
 def kernel_source_hash(root: str) -> str:
     h = hashlib.sha256()
-    for f in ("kvs_kernels.hip", "kvs_device.h"):
+    for f in ("kvs_kernels.hip", "kvs_paged.hip", "kvs_device.h"):
         with open(os.path.join(root, "paper_2609_35750_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
