@@ -173,3 +173,51 @@ def test_long_cache_many_splits(pg):
     seqs = [_seq(e, 8, 2, 128, 90), _seq(inputs.evict_at_layout(3000, 100, 500, 50, "latest_only"), 8, 2, 128, 95)]
     out, _ = _stream(pg, seqs, 16, 2, 128, {2999, 4500, L - 1})
     _check("long", seqs, out, 1.0 / math.sqrt(128))
+
+
+def test_bench_configuration_sampled(pg):
+    """The decode bench.py times: 64 rollouts of the 16k keep-all trace
+    (Hq=32, Hkv=8, D=128) streamed segment by segment through one 16-token
+    block cache, decoded at token 16,383.  Rollouts 0, 31 and 63 carry seeded
+    CPU inputs and are compared with the oracle over R(L-1); the others get
+    seeded GPU noise of the same shape (they share and reuse the block pool)."""
+    dev = torch.device("cuda:0")
+    S, L, p, w, s_, Hq, Hkv, D, bs = 64, 16384, 1024, 4096, 512, 32, 8, 128, 16
+    announce(f"paged bench configuration S={S} L={L} Hq={Hq} Hkv={Hkv} D={D} bs={bs}")
+    e = inputs.evict_at_layout(L, p, w, s_, "keep_all")
+    live = opg.live_set(e, L - 1)
+    max_blocks = (L + bs - 1) // bs + 1
+    nb = S * ((len(live) + w + s_) // bs + 4)
+    cache = pg.PagedKVCache(nb, bs, S, max_blocks, Hkv, D, device=dev)
+    checked = {0: 900, 31: 910, 63: 920}
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(77)
+    ev_t = {}
+    for j, x in enumerate(np.minimum(e, L)):
+        if x < L:
+            ev_t.setdefault(int(x), []).append(j)
+    cuts = sorted(set(ev_t) | {L})
+    kv = {}
+    for sq in range(S):
+        if sq in checked:
+            kv[sq] = (inputs.randn_bf16((L, Hkv, D), checked[sq]), inputs.randn_bf16((L, Hkv, D), checked[sq] + 1))
+        t0 = 0
+        for t1 in cuts:
+            if t0 < t1:
+                if sq in checked:
+                    kn, vn = kv[sq][0][t0:t1].to(dev), kv[sq][1][t0:t1].to(dev)
+                else:
+                    kn = torch.randn((t1 - t0, Hkv, D), generator=gen, device=dev).to(torch.bfloat16)
+                    vn = torch.randn((t1 - t0, Hkv, D), generator=gen, device=dev).to(torch.bfloat16)
+                cache.append(sq, np.arange(t0, t1), kn, vn)
+            if t1 < L:
+                cache.evict(sq, ev_t[t1])
+            t0 = t1
+    q = inputs.randn_bf16((S, Hq, D), 930)
+    o, lse = cache.decode(q.to(dev), 1.0 / math.sqrt(D))
+    o, lse = to_f64(o), to_f64(lse)
+    assert np.all(np.isfinite(o)) and np.all(np.isfinite(lse))
+    for sq in checked:
+        ro, rl = opg.decode(q[sq], kv[sq][0], kv[sq][1], live, 1.0 / math.sqrt(D))
+        assert_close(f"bench-config seq={sq} O", o[sq], ro)
+        assert_close(f"bench-config seq={sq} LSE", lse[sq], rl, max_abs=LSE_ABS, rel_l2=1e-4, elementwise=False)

@@ -222,3 +222,55 @@ def test_paged_abi_validation():
     assert L.kvs_paged_append(FAKE, FAKE, None, FAKE, 4, FAKE, FAKE, FAKE, 8, 16, 2, 64, None) == k.KVS_ERR_NULL
     assert L.kvs_paged_evict(FAKE, -1, FAKE, 8, 16, None) == k.KVS_ERR_SHAPE
     assert L.kvs_paged_evict(None, 3, FAKE, 8, 16, None) == k.KVS_ERR_NULL
+
+
+@needs_lib
+@pytest.mark.parametrize("seed", range(4))
+def test_block_manager_random_operations_match_model(seed):
+    """Random appends, evictions and releases over several sequences against a
+    plain model of the rules (tokens fill the tail of the last block, evicted
+    slots are never refilled, a block is freed when none of its entries is
+    live): live sets, per-sequence block counts and the free-block count agree
+    after every operation, and failed operations change nothing."""
+    from paper_2609_35750_amd.kvs import KvsError
+
+    rng = np.random.default_rng(seed)
+    nb, bs, S, mb = int(rng.integers(6, 20)), int(rng.choice([1, 2, 4, 16])), 3, 8
+    bm = _bm(nb, bs, S, mb)
+    live = [dict() for _ in range(S)]          # position -> slot
+    nxt = [0] * S
+    for _ in range(400):
+        s = int(rng.integers(0, S))
+        op = rng.random()
+        try:
+            if op < 0.55:
+                n = int(rng.integers(1, 2 * bs + 2))
+                pos = list(range(nxt[s], nxt[s] + n))
+                slots = bm.append(s, pos)
+                nxt[s] += n
+                live[s].update(zip(pos, (int(x) for x in slots)))
+            elif op < 0.9 and live[s]:
+                k = int(rng.integers(1, len(live[s]) + 1))
+                pos = [int(x) for x in rng.choice(sorted(live[s]), size=k, replace=False)]
+                slots = bm.evict(s, pos)
+                for p_, sl in zip(pos, slots):
+                    assert live[s].pop(p_) == sl
+            elif op >= 0.9:
+                rel = bm.release(s)
+                assert sorted(rel) == sorted(live[s].values())
+                live[s].clear()
+        except KvsError:
+            pass                                # capacity: the model keeps its state too
+        table, nblk = bm.tables()
+        used = set()
+        for q in range(S):
+            assert bm.live(q) == len(live[q])
+            blocks = set(int(b) for b in table[q, : nblk[q]])
+            # every live slot lies in a listed block; every listed block but the tail holds a live entry
+            assert {sl // bs for sl in live[q].values()} <= blocks
+            assert len(blocks - {sl // bs for sl in live[q].values()}) <= 1
+            assert not (blocks & used)
+            used |= blocks
+        assert len(used) + bm.free_blocks() == nb
+        allslots = [sl for d in live for sl in d.values()]
+        assert len(allslots) == len(set(allslots))
