@@ -208,6 +208,44 @@ def paged_decode_bench(warmup, steps, S=64, block_size=16):
     }
 
 
+def cp_shard_bench(wl, tensors, evict_at, n_shards, warmup, steps, full_ms):
+    """The single-GPU part of context parallelism: the trace's query rows cut
+    into n_shards ranges of about equal work at segment starts, each shard's forward + backward run
+    on its local trace (gathered live keys, then its own tokens) with inputs
+    resident, timed one shard after another.  Reports the slowest shard (the
+    compute time of an n-GPU step, before communication) and the keys the
+    forward's all-gather and the backward's reduce-scatter would move."""
+    import torch
+
+    from paper_2609_35750_amd import inputs, kvs, shard
+
+    dev = torch.device("cuda:0")
+    plans = shard.plan_trace(evict_at, n_shards, inputs.segment_starts(wl.T, wl.p, wl.w, wl.s), balance=True)
+    q, k, v, do = (tensors[x].to(dev) for x in ("q", "k", "v", "do"))
+    times = []
+    for p in plans:
+        idx = torch.from_numpy(p.keys).to(dev)
+        zq = torch.zeros((p.n_g, wl.Hq, wl.D), dtype=q.dtype, device=dev)
+        shp = lambda x: x.contiguous().view(1, p.length, x.shape[1], wl.D)
+        ql, dol = shp(torch.cat([zq, q[p.r0:p.r1]])), shp(torch.cat([zq, do[p.r0:p.r1]]))
+        kl, vl = shp(k.index_select(0, idx)), shp(v.index_select(0, idx))
+        ev = torch.from_numpy(p.evict_local).to(dev).view(1, p.length)
+        o = torch.empty_like(ql)
+        dq, dk, dv = torch.empty_like(ql), torch.empty_like(kl), torch.empty_like(vl)
+        lse = None
+
+        def step():
+            nonlocal lse
+            _, lse = kvs.kvs_evict_attn_fwd(ql, kl, vl, ev, wl.softmax_scale, out=o, lse=lse)
+            kvs.kvs_evict_attn_bwd(dol, ql, kl, vl, o, lse, ev, wl.softmax_scale, dq=dq, dk=dk, dv=dv)
+
+        times.append(time_steps(step, warmup, steps))
+    vol = shard.exchange_volume(plans, wl.Hkv, wl.D)
+    return {"shards": len(plans), "rows": [p.r1 - p.r0 for p in plans], "gathered_keys": [p.n_g for p in plans],
+            "ms_per_shard": [round(t, 4) for t in times], "max_shard_ms": max(times), "full_trace_ms": full_ms,
+            "compute_speedup_vs_one_gpu": full_ms / max(times), "all_gather_bytes_kv": vol["bytes_kv"]}
+
+
 def cpu_baseline(wl, tensors, evict_at, heads=2):
     """The fp64 checker as it stands, timed on q-heads [0, heads) of KV head 0."""
     from oracle import attention as orc
@@ -242,6 +280,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU checker timing")
     ap.add_argument("--no-reprefill", action="store_true", help="skip the re-prefill comparison")
     ap.add_argument("--no-decode", action="store_true", help="skip the paged-cache decode measurement")
+    ap.add_argument("--cp-shards", type=int, default=0,
+                    help="also time the trace cut into this many context-parallel shards (one after another)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (see DESIGN.md for how it would "
@@ -338,6 +378,8 @@ def main():
     roofline["frac_of_measured_peak"] = achieved / measured_peak
     if not args.no_reprefill:
         out["reprefill"] = reprefill_compare(wl, kvs, args.warmup, args.steps, ms_per_step)
+    if args.cp_shards > 0 and not wl.varlen:
+        out["cp_shards"] = cp_shard_bench(wl, tensors, e, args.cp_shards, args.warmup, args.steps, ms_per_step)
     if not args.no_decode:
         out["paged_decode"] = paged_decode_bench(args.warmup, args.steps)
     if not args.no_cpu:
