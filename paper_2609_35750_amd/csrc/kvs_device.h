@@ -181,25 +181,46 @@ __device__ __forceinline__ const T* uniform_ptr(const T* p) {
   return (const T*)(uintptr_t)(((uint64_t)hi << 32) | lo);
 }
 
-// LDS tile of rows x D bf16.  Rows are padded (D = 128: 144 elements, D = 64:
-// 72) and, for D = 128, the lowest bit of the 16-byte chunk index is flipped
-// in rows 8..15 of every 16.  Two access patterns are then free of bank
-// conflicts: 16 lanes reading the same chunk of 16 consecutive rows (b128 reads
-// of MFMA operands), and the 4-row x 32-byte block of each 16-lane group of a
-// transposed read.  Because the flip only touches bit 0 of the chunk index and
-// depends only on the row modulo 16, moving by whole k-steps (32 bytes), by
-// 32-column blocks or by 16-row blocks is a constant offset, so every operand
-// read is a per-lane base plus an immediate.
-template <int D>
+// LDS tile of rows x D bf16 with padded rows and a per-row XOR on the
+// 16-byte chunk index ("swizzle").  The hardware serves a b128 read 16 lanes
+// at a time and a b64 read (the transposed operand reads) 32 lanes at a time,
+// each group 256 bytes over the 64 four-byte banks, so two patterns must be
+// conflict-free: 16 lanes reading one chunk of 16 consecutive rows (b128 MFMA
+// operands) and 32 lanes reading a 4-row x 64-byte block (transposed reads).
+//   attention tiles, D = 128: pitch 160 elements (20 chunks, 4 of them
+//     padding), chunk ^= (r / 4) % 4.  Row r starts at bank 16 r (mod 64), so
+//     4 consecutive rows cover all banks with 64 bytes each, and the XOR
+//     spreads the 16 rows of a b128 group over 16 distinct 4-bank groups.
+//   decode tiles (COMPACT), D = 128: pitch 144, chunk ^= (r / 8) % 2: b128
+//     reads are conflict-free, transposed reads two-way conflicted; it keeps
+//     a decode wave's double-buffered tiles within a quarter of the LDS.
+//   D = 64: pitch 72, no swizzle.
+// The swizzle touches only bits 0-1 of the chunk index and depends only on
+// the row modulo 16, so moving by two k-steps (64 bytes), by 32-column blocks
+// or by 16-row blocks is a constant offset: a b128 operand read is one of two
+// per-lane bases (even or odd k-step) plus an immediate, a transposed read a
+// per-lane base plus an immediate.
+template <int D, bool COMPACT = false>
 struct Lay {
-  static constexpr int PITCH = D == 128 ? 144 : 72;   // bf16 elements per LDS row
-  static constexpr int CPR = D / 8;                    // 16-byte data chunks per row
-  static constexpr int CPRP = PITCH / 8;               // chunks per padded row
-  __device__ static __forceinline__ int flip(int r) { return D == 128 ? ((r >> 3) & 1) : 0; }
+  static constexpr int PITCH = D == 128 ? (COMPACT ? 144 : 160) : 72;   // bf16 elements per LDS row
+  static constexpr int CPR = D / 8;                                   // 16-byte data chunks per row
+  static constexpr int CPRP = PITCH / 8;                              // chunks per padded row
+  __device__ static __forceinline__ int flip(int r) {
+    return D == 128 ? (COMPACT ? ((r >> 3) & 1) : ((r >> 2) & 3)) : 0;
+  }
   __device__ static __forceinline__ int off(int r, int col) { return r * PITCH + (((col >> 3) ^ flip(r)) << 3) + (col & 7); }
-  // b128 operand read of row (row0 + l % 32), columns 8 (l / 32) .. +7 of k-step 0;
-  // add row0 * PITCH + 16 ks (row0 a multiple of 16).
-  __device__ static __forceinline__ int row_lane(int lane) { return off(lane & 31, 8 * (lane >> 5)); }
+  // b128 operand reads: row (row0 + l % 32), columns 16 ks + 8 (l / 32) .. +7.
+  // (odd k-steps: chunk bit 1 toggled, i.e. the base XOR 16, since rows
+  // start at multiples of 32 elements)
+  struct RowLane {
+    int even;   // base of k-step 0 (row0 = 0)
+  };
+  __device__ static __forceinline__ RowLane row_lane(int lane) { return {off(lane & 31, 8 * (lane >> 5))}; }
+  // element offset of k-step ks (add row0 * PITCH, row0 a multiple of 16)
+  __device__ static __forceinline__ int row_at(RowLane rl, int ks) {
+    const int odd = (D == 128 && !COMPACT) ? (rl.even ^ 16) : rl.even + 16;
+    return (ks & 1 ? odd : rl.even) + 32 * (ks >> 1);
+  }
   // transposed operand reads (see tr_operand): rows 4 (g16 / 2) + (li / 4) and +8,
   // columns 16 (g16 % 2) + 4 (li % 4); add row0 * PITCH + c0 (row0 % 16 == 0, c0 % 32 == 0).
   __device__ static __forceinline__ int tr_lo(int lane) {
@@ -215,10 +236,10 @@ struct Lay {
 // A operand of a 32x32x16 MFMA read transposed from an LDS tile: rows
 // (contraction index) row0 + 4 half + {0..3} and row0 + 8 + 4 half + {0..3}
 // (the order in which the C layout of a score block lists its 16 values),
-// columns c0 + (l % 32).  tl, th = Lay<D>::tr_lo(lane), tr_hi(lane).
-template <int D>
+// columns c0 + (l % 32).  tl, th = Lay<D, COMPACT>::tr_lo(lane), tr_hi(lane).
+template <int D, bool COMPACT = false>
 __device__ __forceinline__ bf16x8 tr_operand(const uint16_t* tile, int row0, int c0, int tl, int th) {
-  const int o = row0 * Lay<D>::PITCH + c0;
+  const int o = row0 * Lay<D, COMPACT>::PITCH + c0;
   return cat_tr(lds_read_tr(tile + tl + o), lds_read_tr(tile + th + o));
 }
 
@@ -232,24 +253,27 @@ __device__ __forceinline__ bf16x8 tr_operand(const uint16_t* tile, int row0, int
 // min(row0 + r, rmax) (rows past the end of a trace repeat its last row;
 // callers mask them).  Lanes whose slot is row padding copy the row's first
 // chunk into it (padding is never read), so no lane is switched off.
-template <int D, int R, int MAXI>
+template <int D, int R, int MAXI, bool COMPACT = false>
 struct RowStager {
-  using LY = Lay<D>;
+  using LY = Lay<D, COMPACT>;
   static constexpr int NI = R * LY::CPRP / kWave;   // 64-slot pieces per tile
   static_assert(R * LY::CPRP % kWave == 0, "tile must fill whole 64-slot pieces");
-  int row[MAXI];        // tile row of this lane's slot, or -1 (no piece)
-  int col[MAXI];        // element column of the slot's first element in the source row
   uint32_t off[MAXI];   // byte offset of the slot's source from the tile's first row (no clamping)
 
+  // tile row and source element column of this lane's slot in piece n
+  __device__ static __forceinline__ void slot(int n, int lane, int& r, int& col) {
+    const int q = n * kWave + lane;
+    r = q / LY::CPRP;
+    const int pc = q - r * LY::CPRP;
+    col = pc < LY::CPR ? 8 * (pc ^ LY::flip(r)) : 0;
+  }
   __device__ __forceinline__ void init(int wave, int nw, int lane, long long row_stride) {
 #pragma unroll
     for (int i = 0; i < MAXI; ++i) {
       const int n = wave + i * nw;
-      const int q = n * kWave + lane;
-      const int r = q / LY::CPRP, pc = q - r * LY::CPRP;
-      row[i] = n < NI ? r : -1;
-      col[i] = (n < NI && pc < LY::CPR) ? 8 * (pc ^ LY::flip(r)) : 0;
-      off[i] = n < NI ? (uint32_t)(r * row_stride + col[i]) * 2u : 0u;
+      int r, col;
+      slot(n, lane, r, col);
+      off[i] = n < NI ? (uint32_t)(r * row_stride + col) * 2u : 0u;
     }
   }
   // number of copy instructions one call of issue() makes for this wave
@@ -266,12 +290,15 @@ struct RowStager {
         if (n < NI) dma_b128(base, off[i], lds + n * kWave * 16);
       }
     } else {
+      const int lane = threadIdx.x & (kWave - 1);
 #pragma unroll
       for (int i = 0; i < MAXI; ++i) {
         const int n = wave + i * nw;
         if (n < NI) {
-          const int dr = min(row0 + row[i], rmax) - row0;
-          dma_b128(base, (uint32_t)(dr * row_stride + col[i]) * 2u, lds + n * kWave * 16);
+          int r, col;
+          slot(n, lane, r, col);
+          const int dr = min(row0 + r, rmax) - row0;
+          dma_b128(base, (uint32_t)(dr * row_stride + col) * 2u, lds + n * kWave * 16);
         }
       }
     }

@@ -183,13 +183,15 @@ __device__ __forceinline__ int walker_next(TileWalker& w, const int2* __restrict
 
 // ---------------------------------------------------------------- operand reads from swizzled tiles
 // S^T block (32 keys x 32 queries) of the current tile: A = K rows from LDS, B = Q^T in registers.
-// rl = Lay<D>::row_lane(lane).
-template <int D>
-__device__ __forceinline__ f32x16 scores_t(const uint16_t* tile, int row0, const bf16x8* breg, int rl) {
+// rl = Lay<D, COMPACT>::row_lane(lane).
+template <int D, bool COMPACT = false>
+__device__ __forceinline__ f32x16 scores_t(const uint16_t* tile, int row0, const bf16x8* breg,
+                                           typename Lay<D, COMPACT>::RowLane rl) {
+  using LY = Lay<D, COMPACT>;
   f32x16 s = {};
-  const uint16_t* base = tile + rl + row0 * Lay<D>::PITCH;
+  const uint16_t* base = tile + row0 * LY::PITCH;
 #pragma unroll
-  for (int ks = 0; ks < D / 16; ++ks) s = mfma32(lds_read_b128(base + 16 * ks), breg[ks], s);
+  for (int ks = 0; ks < D / 16; ++ks) s = mfma32(lds_read_b128(base + LY::row_at(rl, ks)), breg[ks], s);
   return s;
 }
 
@@ -237,9 +239,10 @@ __device__ __forceinline__ bool row_tile(const RowArgs& a, RowTile& t) {
   return true;
 }
 
-// Asynchronous staging of one 64-key K/V (and evict_at) tile of KV head g.
+// Asynchronous staging of one 64-key K/V (and evict_at) tile of KV head g
+// (compact layout: two workgroups of the dQ kernel share a CU).
 template <int D>
-using KVStager = RowStager<D, kKeyTile, (kKeyTile * Lay<D>::CPRP / kWave + 3) / 4>;   // >= 4 waves
+using KVStager = RowStager<D, kKeyTile, (kKeyTile * Lay<D, true>::CPRP / kWave + 3) / 4, true>;   // >= 4 waves
 
 template <int D>
 __device__ __forceinline__ void stage_kv(const KVStager<D>& st, uint16_t* sK, uint16_t* sV, int* sE, const RowArgs& a,
@@ -266,16 +269,16 @@ template <int D>
 constexpr int fwd_bn() { return D == 128 ? 32 : 64; }
 
 template <int D>
-using FwdStager = RowStager<D, fwd_bn<D>(), (fwd_bn<D>() * Lay<D>::CPRP / kWave + 3) / 4>;   // >= 4 waves
+using FwdStager = RowStager<D, fwd_bn<D>(), (fwd_bn<D>() * Lay<D, true>::CPRP / kWave + 3) / 4, true>;   // >= 4 waves
 
 template <int D>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 128 ? 3 : 2, D == 128 ? 3 : 2)))
 fwd_kernel(RowArgs a) {
   constexpr int KS = D / 16, DB = D / 32, BN = fwd_bn<D>(), NKB = BN / 32, NSUB = kKeyTile / BN;
-  __shared__ __attribute__((aligned(1024))) uint16_t sK0[BN * Lay<D>::PITCH];
-  __shared__ __attribute__((aligned(1024))) uint16_t sK1[BN * Lay<D>::PITCH];
-  __shared__ __attribute__((aligned(1024))) uint16_t sV0[BN * Lay<D>::PITCH];
-  __shared__ __attribute__((aligned(1024))) uint16_t sV1[BN * Lay<D>::PITCH];
+  __shared__ __attribute__((aligned(1024))) uint16_t sK0[BN * Lay<D, true>::PITCH];
+  __shared__ __attribute__((aligned(1024))) uint16_t sK1[BN * Lay<D, true>::PITCH];
+  __shared__ __attribute__((aligned(1024))) uint16_t sV0[BN * Lay<D, true>::PITCH];
+  __shared__ __attribute__((aligned(1024))) uint16_t sV1[BN * Lay<D, true>::PITCH];
   __shared__ __attribute__((aligned(256))) int sE0[BN];
   __shared__ __attribute__((aligned(256))) int sE1[BN];
 
@@ -286,7 +289,8 @@ fwd_kernel(RowArgs a) {
   const Trace tr = rt.tr;
   const int i = rt.i0w + col;
   const bool row_ok = i < tr.L;
-  const int rl = Lay<D>::row_lane(lane), tl = Lay<D>::tr_lo(lane), th = Lay<D>::tr_hi(lane);
+  const auto rl = Lay<D, true>::row_lane(lane);
+  const int tl = Lay<D, true>::tr_lo(lane), th = Lay<D, true>::tr_hi(lane);
   FwdStager<D> kvst;
   kvst.init(wave, nw, lane, (long long)a.Hkv * D);
   // asynchronous staging of sub-tile (kt, sub) of KV head g
@@ -340,7 +344,7 @@ fwd_kernel(RowArgs a) {
       f32x16 s[NKB];
 #pragma unroll
       for (int kb = 0; kb < NKB; ++kb) {
-        s[kb] = scores_t<D>(cK, 32 * kb, qreg, rl);
+        s[kb] = scores_t<D, true>(cK, 32 * kb, qreg, rl);
         if (cls == kPartial) mask_t(s[kb], cE, kb, j0, i, tr.L, half);
       }
       float mx = -INFINITY;
@@ -380,7 +384,7 @@ fwd_kernel(RowArgs a) {
           const bf16x8 pb = pack8(s[kb], 8 * t);
 #pragma unroll
           for (int d = 0; d < DB; ++d)
-            acc[d] = mfma32(tr_operand<D>(cV, 32 * kb + 16 * t, 32 * d, tl, th), pb, acc[d]);
+            acc[d] = mfma32(tr_operand<D, true>(cV, 32 * kb + 16 * t, 32 * d, tl, th), pb, acc[d]);
         }
     }
     wait_vm();
@@ -416,7 +420,7 @@ fwd_kernel(RowArgs a) {
   }
 }
 
-// ---------------------------------------------------------------- backward: Delta = rowsum(dO * O)
+// ---------------------------------------------------------------- backward: Delta = rowsum(dO * O), stored as -Delta
 // Also writes LSE * log2(e), the form in which the backward kernels use it.
 template <int D>
 __global__ void __launch_bounds__(256) bwd_pre_kernel(const uint16_t* __restrict__ o, const uint16_t* __restrict__ dout,
@@ -441,7 +445,7 @@ __global__ void __launch_bounds__(256) bwd_pre_kernel(const uint16_t* __restrict
   if (ok && sub == 0) {
     const int tok = (int)(row / Hq), h = (int)(row % Hq);
     const long long idx = varlen ? (long long)h * ntok + tok : ((long long)(tok / T) * Hq + h) * T + tok % T;
-    delta[idx] = s;
+    delta[idx] = -s;   // stored negated: both backward kernels add it
     lse2[idx] = lse[idx] * 1.4426950408889634f;
   }
 }
@@ -450,10 +454,10 @@ __global__ void __launch_bounds__(256) bwd_pre_kernel(const uint16_t* __restrict
 template <int D>
 __global__ void __launch_bounds__(512) dq_kernel(RowArgs a) {
   constexpr int KS = D / 16, DB = D / 32;
-  __shared__ __attribute__((aligned(1024))) uint16_t sK0[kKeyTile * Lay<D>::PITCH];
-  __shared__ __attribute__((aligned(1024))) uint16_t sK1[kKeyTile * Lay<D>::PITCH];
-  __shared__ __attribute__((aligned(1024))) uint16_t sV0[kKeyTile * Lay<D>::PITCH];
-  __shared__ __attribute__((aligned(1024))) uint16_t sV1[kKeyTile * Lay<D>::PITCH];
+  __shared__ __attribute__((aligned(1024))) uint16_t sK0[kKeyTile * Lay<D, true>::PITCH];
+  __shared__ __attribute__((aligned(1024))) uint16_t sK1[kKeyTile * Lay<D, true>::PITCH];
+  __shared__ __attribute__((aligned(1024))) uint16_t sV0[kKeyTile * Lay<D, true>::PITCH];
+  __shared__ __attribute__((aligned(1024))) uint16_t sV1[kKeyTile * Lay<D, true>::PITCH];
   __shared__ __attribute__((aligned(256))) int sE0[kKeyTile];
   __shared__ __attribute__((aligned(256))) int sE1[kKeyTile];
 
@@ -464,13 +468,14 @@ __global__ void __launch_bounds__(512) dq_kernel(RowArgs a) {
   const Trace tr = rt.tr;
   const int i = rt.i0w + col;
   const bool row_ok = i < tr.L;
-  const int rl = Lay<D>::row_lane(lane), tl = Lay<D>::tr_lo(lane), th = Lay<D>::tr_hi(lane);
+  const auto rl = Lay<D, true>::row_lane(lane);
+  const int tl = Lay<D, true>::tr_lo(lane), th = Lay<D, true>::tr_hi(lane);
   KVStager<D> kvst;
   kvst.init(wave, nw, lane, (long long)a.Hkv * D);
   const int ic = min(i, tr.L - 1);
 
   bf16x8 qreg[KS], oreg[KS];
-  float lse2, dlt;
+  float lse2, ndlt;
   {
     const size_t roff = ((size_t)(tr.tok0 + ic) * a.Hq + rt.h) * D + 8 * half;
 #pragma unroll
@@ -480,7 +485,7 @@ __global__ void __launch_bounds__(512) dq_kernel(RowArgs a) {
     }
     const long long li = lse_index(a.varlen, a.ntok, a.Hq, a.T, rt.b, rt.h, tr.tok0, ic);
     lse2 = a.lse_in[li];   // already scaled by log2(e)
-    dlt = a.delta[li];
+    ndlt = a.delta[li];   // -Delta
   }
 
   f32x16 acc[DB];
@@ -507,20 +512,20 @@ __global__ void __launch_bounds__(512) dq_kernel(RowArgs a) {
     if (cls != kEmpty) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
-        f32x16 s = scores_t<D>(cK, 32 * kb, qreg, rl);
+        f32x16 s = scores_t<D, true>(cK, 32 * kb, qreg, rl);
         if (cls == kPartial) mask_t(s, cE, kb, j0, i, tr.L, half);
-        const f32x16 dp = scores_t<D>(cV, 32 * kb, oreg, rl);
+        const f32x16 dp = scores_t<D, true>(cV, 32 * kb, oreg, rl);
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], a.scale_log2, -lse2));
-          s[r] = p * (dp[r] - dlt);
+          s[r] = p * (dp[r] + ndlt);
         }
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
           const bf16x8 dsb = pack8(s, 8 * t);
 #pragma unroll
           for (int d = 0; d < DB; ++d)
-            acc[d] = mfma32(tr_operand<D>(cK, 32 * kb + 16 * t, 32 * d, tl, th), dsb, acc[d]);
+            acc[d] = mfma32(tr_operand<D, true>(cK, 32 * kb + 16 * t, 32 * d, tl, th), dsb, acc[d]);
         }
       }
     }
@@ -606,7 +611,8 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
   const int jc = min(j, tr.L - 1);
   const int ej = key_ok ? min(a.evict[tr.tok0 + j], tr.L) : 0;
   const unsigned kspan = key_ok ? (unsigned)(ej - j) : 0u;   // rows j .. ej - 1 see this key
-  const int rl = Lay<D>::row_lane(lane), tl = Lay<D>::tr_lo(lane), th = Lay<D>::tr_hi(lane);
+  const auto rl = Lay<D>::row_lane(lane);
+  const int tl = Lay<D>::tr_lo(lane), th = Lay<D>::tr_hi(lane);
   int emin_w = key_ok ? ej : INT_MAX, emax_w = key_ok ? ej : INT_MIN;
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) {
@@ -665,7 +671,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
                         f16x8 (&ph)[2]) __attribute__((always_inline)) {
     f32x16 x = {};
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) x = mfma32(lds_read_b128(cQ + rl + rb * PITCH + 16 * ks), kvreg[ks], x);
+    for (int ks = 0; ks < KS; ++ks) x = mfma32(lds_read_b128(cQ + rb * PITCH + Lay<D>::row_at(rl, ks)), kvreg[ks], x);
 #pragma unroll
     for (int q4 = 0; q4 < 4; ++q4) {
       const float4 l4 = *reinterpret_cast<const float4*>(cL + rb + 8 * q4 + 4 * half);
@@ -697,13 +703,13 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
 #pragma unroll
     for (int q4 = 0; q4 < 4; ++q4) {
       const float4 d4 = *reinterpret_cast<const float4*>(cD + rb + 8 * q4 + 4 * half);
-      dp[4 * q4] = -d4.x;
-      dp[4 * q4 + 1] = -d4.y;
-      dp[4 * q4 + 2] = -d4.z;
-      dp[4 * q4 + 3] = -d4.w;
+      dp[4 * q4] = d4.x;   // -Delta
+      dp[4 * q4 + 1] = d4.y;
+      dp[4 * q4 + 2] = d4.z;
+      dp[4 * q4 + 3] = d4.w;
     }
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) dp = mfma32(lds_read_b128(cO + rl + rb * PITCH + 16 * ks), kvreg[ks], dp);
+    for (int ks = 0; ks < KS; ++ks) dp = mfma32(lds_read_b128(cO + rb * PITCH + Lay<D>::row_at(rl, ks)), kvreg[ks], dp);
     const f16x8 p0 = *xp0, p1 = *xp1;
     f32x16 x;
 #pragma unroll
@@ -726,7 +732,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk) {
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) qa[blk][ks] = lds_read_b128(cQ + rl + 32 * blk * PITCH + 16 * ks);
+      for (int ks = 0; ks < KS; ++ks) qa[blk][ks] = lds_read_b128(cQ + 32 * blk * PITCH + Lay<D>::row_at(rl, ks));
 #pragma unroll
       for (int q4 = 0; q4 < 4; ++q4) lv[blk][q4] = *reinterpret_cast<const float4*>(cL + 32 * blk + 8 * q4 + 4 * half);
     }
@@ -790,7 +796,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) oa[blk][ks] = lds_read_b128(cO + rl + 32 * blk * PITCH + 16 * ks);
+      for (int ks = 0; ks < KS; ++ks) oa[blk][ks] = lds_read_b128(cO + 32 * blk * PITCH + Lay<D>::row_at(rl, ks));
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk) {
 #pragma unroll
@@ -801,7 +807,13 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk) {
-      dp[blk] = f32x16{};
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {   // start at -Delta, so the product gives dP - Delta
+        dp[blk][4 * q4] = dv4[blk][q4].x;
+        dp[blk][4 * q4 + 1] = dv4[blk][q4].y;
+        dp[blk][4 * q4 + 2] = dv4[blk][q4].z;
+        dp[blk][4 * q4 + 3] = dv4[blk][q4].w;
+      }
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) dp[blk] = mfma32(oa[blk][ks], kvreg[ks], dp[blk]);
     }
@@ -816,14 +828,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
     for (int blk = 0; blk < 2; ++blk) {
       f32x16 x;
 #pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        const float dq[4] = {dv4[blk][q4].x, dv4[blk][q4].y, dv4[blk][q4].z, dv4[blk][q4].w};
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          const int r = 4 * q4 + t;
-          x[r] = (float)pr[blk][r >> 3][r & 7] * (dp[blk][r] - dq[t]);
-        }
-      }
+      for (int r = 0; r < 16; ++r) x[r] = (float)pr[blk][r >> 3][r & 7] * dp[blk][r];
       sb[blk][0] = pack8(x, 0);
       sb[blk][1] = pack8(x, 8);
       if (blk == 0) {
@@ -1149,7 +1154,7 @@ size_t ws_kstats_bytes(int B, int ntok) {
   return (n * sizeof(int2) + 255) & ~(size_t)255;
 }
 
-// Delta followed by LSE * log2(e), each [Hq][ntok] (or [B][Hq][T]) fp32.
+// -Delta followed by LSE * log2(e), each [Hq][ntok] (or [B][Hq][T]) fp32.
 size_t ws_delta_bytes(int Hq, int ntok) { return 2 * (((size_t)Hq * ntok * sizeof(float) + 255) & ~(size_t)255); }
 
 static size_t round256(size_t n) { return (n + 255) & ~(size_t)255; }

@@ -76,7 +76,7 @@ constexpr int kDecTile = 32;   // cache slots per tile
 // row, 9 pieces of 64 lanes; D = 64: 9 per row, 4.5 pieces -> 5 with a guard).
 template <int D>
 struct GatherStager {
-  using LY = Lay<D>;
+  using LY = Lay<D, true>;
   static constexpr int SLOTS = kDecTile * LY::CPRP;
   static constexpr int NI = (SLOTS + kWave - 1) / kWave;
   int row[NI];   // tile row of this lane's 16-byte slot (-1: none)
@@ -139,7 +139,7 @@ __device__ __forceinline__ void wait_vm_le() {
 // of them, since it cannot see them.)
 template <int D>
 __global__ void __launch_bounds__(64) paged_decode_kernel(DecodeArgs a) {
-  constexpr int KS = D / 16, DB = D / 32, PITCH = Lay<D>::PITCH, TILE = kDecTile * PITCH, R = kDecRing;
+  constexpr int KS = D / 16, DB = D / 32, PITCH = Lay<D, true>::PITCH, TILE = kDecTile * PITCH, R = kDecRing;
   constexpr int OPS_KV = 2 * GatherStager<D>::NI;   // K and V copy instructions per tile
   constexpr int OPS_STEP = OPS_KV + 2;             // plus the table and slot_pos copies
   static_assert((R - 1) * OPS_STEP < 64, "outstanding copies must fit vmcnt");
@@ -154,7 +154,8 @@ __global__ void __launch_bounds__(64) paged_decode_kernel(DecodeArgs a) {
   const int g = wg % a.Hkv;
   const int s = wg / a.Hkv;
   const int lane = threadIdx.x, half = lane >> 5, col = lane & 31;
-  const int rl = Lay<D>::row_lane(lane), tl = Lay<D>::tr_lo(lane), th = Lay<D>::tr_hi(lane);
+  const auto rl = Lay<D, true>::row_lane(lane);
+  const int tl = Lay<D, true>::tr_lo(lane), th = Lay<D, true>::tr_hi(lane);
 
   // blocks in use by sequence s (clamped to the table width; some slots may be evicted)
   const int nslots = min(max(a.nblk[s], 0), a.max_blocks) * a.BS;
@@ -227,7 +228,7 @@ __global__ void __launch_bounds__(64) paged_decode_kernel(DecodeArgs a) {
         f32x16 sc = f32x16{};
         bf16x8 ka[KS];
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) ka[ks] = lds_read_b128(cK + rl + 16 * ks);
+        for (int ks = 0; ks < KS; ++ks) ka[ks] = lds_read_b128(cK + Lay<D, true>::row_at(rl, ks));
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) sc = mfma32(ka[ks], qreg[ks], sc);
         // element r <-> tile row 8 (r / 4) + 4 half + r % 4
@@ -259,7 +260,7 @@ __global__ void __launch_bounds__(64) paged_decode_kernel(DecodeArgs a) {
         for (int t2 = 0; t2 < 2; ++t2) {
           const bf16x8 pb = pack8(sc, 8 * t2);
 #pragma unroll
-          for (int d = 0; d < DB; ++d) acc[d] = mfma32(tr_operand<D>(cV, 16 * t2, 32 * d, tl, th), pb, acc[d]);
+          for (int d = 0; d < DB; ++d) acc[d] = mfma32(tr_operand<D, true>(cV, 16 * t2, 32 * d, tl, th), pb, acc[d]);
         }
       }
     }
