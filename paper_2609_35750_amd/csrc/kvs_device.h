@@ -187,13 +187,14 @@ __device__ __forceinline__ const T* uniform_ptr(const T* p) {
 // each group 256 bytes over the 64 four-byte banks, so two patterns must be
 // conflict-free: 16 lanes reading one chunk of 16 consecutive rows (b128 MFMA
 // operands) and 32 lanes reading a 4-row x 64-byte block (transposed reads).
-//   attention tiles, D = 128: pitch 160 elements (20 chunks, 4 of them
+//   wide (dK/dV tiles), D = 128: pitch 160 elements (20 chunks, 4 of them
 //     padding), chunk ^= (r / 4) % 4.  Row r starts at bank 16 r (mod 64), so
 //     4 consecutive rows cover all banks with 64 bytes each, and the XOR
 //     spreads the 16 rows of a b128 group over 16 distinct 4-bank groups.
-//   decode tiles (COMPACT), D = 128: pitch 144, chunk ^= (r / 8) % 2: b128
-//     reads are conflict-free, transposed reads two-way conflicted; it keeps
-//     a decode wave's double-buffered tiles within a quarter of the LDS.
+//   COMPACT (forward, dQ and decode tiles), D = 128: pitch 144, chunk ^=
+//     (r / 8) % 2: b128 reads are conflict-free, transposed reads two-way
+//     conflicted; 11% less LDS, which keeps two dQ workgroups on a CU and a
+//     decode wave's double-buffered tiles within a quarter of the LDS.
 //   D = 64: pitch 72, no swizzle.
 // The swizzle touches only bits 0-1 of the chunk index and depends only on
 // the row modulo 16, so moving by two k-steps (64 bytes), by 32-column blocks
