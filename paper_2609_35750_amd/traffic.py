@@ -30,11 +30,25 @@ KERNELS = {"fwd_kernel": "fwd", "dkdv_kernel": "bwd_dkdv", "dq_kernel": "bwd_dq"
            "kstats_kernel": "classify", "paged_decode_kernel": "paged_decode"}
 
 
+def _code_only(text: str) -> str:
+    """Source without // comments, trailing blanks and empty lines: edits to
+    comments do not change the kernels the counters were taken on."""
+    out = []
+    for line in text.splitlines():
+        i = line.find("//")
+        if i >= 0:
+            line = line[:i]
+        line = line.rstrip()
+        if line:
+            out.append(line)
+    return "\n".join(out)
+
+
 def kernel_source_hash(root: str) -> str:
     h = hashlib.sha256()
     for f in ("kvs_kernels.hip", "kvs_paged.hip", "kvs_device.h"):
-        with open(os.path.join(root, "paper_2609_35750_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(root, "paper_2609_35750_amd", "csrc", f), encoding="utf-8") as fh:
+            h.update(_code_only(fh.read()).encode())
     return h.hexdigest()[:16]
 
 
