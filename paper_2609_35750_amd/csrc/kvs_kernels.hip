@@ -186,9 +186,8 @@ __device__ __forceinline__ int walker_next(TileWalker& w, const int2* __restrict
 // rl = Lay<D, COMPACT>::row_lane(lane).
 template <int D, bool COMPACT = false>
 __device__ __forceinline__ f32x16 scores_t(const uint16_t* tile, int row0, const bf16x8* breg,
-                                           typename Lay<D, COMPACT>::RowLane rl) {
+                                           typename Lay<D, COMPACT>::RowLane rl, f32x16 s = f32x16{}) {
   using LY = Lay<D, COMPACT>;
-  f32x16 s = {};
   const uint16_t* base = tile + row0 * LY::PITCH;
 #pragma unroll
   for (int ks = 0; ks < D / 16; ++ks) s = mfma32(lds_read_b128(base + LY::row_at(rl, ks)), breg[ks], s);
@@ -519,11 +518,15 @@ __global__ void __launch_bounds__(512) dq_kernel(RowArgs a) {
       for (int kb = 0; kb < 2; ++kb) {
         f32x16 s = scores_t<D, true>(cK, 32 * kb, qreg, rl);
         if (cls == kPartial) mask_t(s, cE, kb, j0, i, tr.L, half);
-        const f32x16 dp = scores_t<D, true>(cV, 32 * kb, oreg, rl);
+        // dP - Delta: the product starts at -Delta
+        f32x16 d0;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) d0[r] = ndlt;
+        const f32x16 dp = scores_t<D, true>(cV, 32 * kb, oreg, rl, d0);
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], a.scale_log2, -lse2));
-          s[r] = p * (dp[r] + ndlt);
+          s[r] = p * dp[r];
         }
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
