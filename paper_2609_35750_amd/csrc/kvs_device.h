@@ -114,18 +114,6 @@ __device__ __forceinline__ float halves_sum(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// acc + sum of the eight bf16 values of p (v_dot2 with ones: two values per instruction)
-__device__ __forceinline__ float add_bf16x8(float acc, bf16x8 p) {
-  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-  const bf16x2 one = {(__bf16)1.f, (__bf16)1.f};
-#pragma unroll
-  for (int e = 0; e < 8; e += 2) {
-    const bf16x2 v = {p[e], p[e + 1]};
-    acc = __builtin_amdgcn_fdot2_f32_bf16(v, one, acc, false);
-  }
-  return acc;
-}
-
 // Asynchronous global -> LDS copy (global_load_lds_dword{,x4}): lane l of the
 // wave writes its 4 or 16 bytes at LDS byte address lds + (4 or 16) l.  Issued
 // through inline assembly so that the compiler does not count the copy as an
@@ -277,8 +265,6 @@ struct RowStager {
       off[i] = n < NI ? (uint32_t)(r * row_stride + col) * 2u : 0u;
     }
   }
-  // number of copy instructions one call of issue() makes for this wave
-  __device__ static __forceinline__ int count(int wave, int nw) { return wave < NI ? (NI - 1 - wave) / nw + 1 : 0; }
   // row0 <= rmax; rows row0 .. row0 + R - 1 of g (clamped) span less than 4 GiB; row_stride as given to init().
   // lds: LDS byte address of the tile (lds_addr).
   __device__ __forceinline__ void issue(uint32_t lds, const uint16_t* __restrict__ g, long long row_stride, int row0,
@@ -314,18 +300,5 @@ __device__ __forceinline__ void stage_words(uint32_t lds, const void* __restrict
 
 // Wait for this wave's outstanding global loads (including LDS-direct ones).
 __device__ __forceinline__ void wait_vm() { __builtin_amdgcn_s_waitcnt(0x0F70); }
-
-// Wait until at most n of this wave's vector memory operations are outstanding
-// (they complete in issue order, so everything issued before the last n is done).
-__device__ __forceinline__ void wait_vm_upto(int n) {
-  switch (n) {
-#define KVS_VM_CASE(k) case k: __builtin_amdgcn_s_waitcnt(0x0F70 | k); break;
-    KVS_VM_CASE(1) KVS_VM_CASE(2) KVS_VM_CASE(3) KVS_VM_CASE(4) KVS_VM_CASE(5) KVS_VM_CASE(6) KVS_VM_CASE(7)
-    KVS_VM_CASE(8) KVS_VM_CASE(9) KVS_VM_CASE(10) KVS_VM_CASE(11) KVS_VM_CASE(12) KVS_VM_CASE(13) KVS_VM_CASE(14)
-    KVS_VM_CASE(15)
-#undef KVS_VM_CASE
-    default: __builtin_amdgcn_s_waitcnt(0x0F70); break;
-  }
-}
 
 }  // namespace kvs
