@@ -286,8 +286,8 @@ def main():
                     help="also time the trace cut into this many context-parallel shards (one after another)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path (see DESIGN.md for how it would "
-              "shard); run with --gpus 1", file=sys.stderr)
+        print("bench.py measures one GPU: the library has no multi-GPU path (--cp-shards N times the "
+              "context-parallel shards of the trace one after another on one GPU); run with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
     import torch
