@@ -248,20 +248,24 @@ def cp_shard_bench(wl, tensors, evict_at, n_shards, warmup, steps, full_ms):
             "compute_speedup_vs_one_gpu": full_ms / max(times), "all_gather_bytes_kv": vol["bytes_kv"]}
 
 
-def cpu_baseline(wl, tensors, evict_at, heads=2):
-    """The fp64 checker as it stands, timed on q-heads [0, heads) of KV head 0."""
+def cpu_baseline(wl, tensors, evict_at, min_seconds=10.0):
+    """The fp64 checker as it stands, timed one q-head at a time (with its KV
+    head) over the whole workload until at least `min_seconds` have passed."""
     from oracle import attention as orc
 
-    G = wl.G
-    heads = min(heads, G)
-    q = tensors["q"][:, :heads]
-    k, v = tensors["k"][:, :1], tensors["v"][:, :1]
-    do = tensors["do"][:, :heads]
     cu = wl.cu_seqlens() if wl.varlen else None
-    t0 = time.perf_counter()
-    orc.backward(q, k, v, evict_at, wl.softmax_scale, do, cu_seqlens=cu)
-    dt = time.perf_counter() - t0
-    flops = 14 * wl.D * heads * visible_pairs(evict_at, wl.lengths)
+    per_head = visible_pairs(evict_at, wl.lengths)
+    heads, dt = 0, 0.0
+    while heads < wl.Hq and dt < min_seconds:
+        h = heads
+        g = h // wl.G
+        sl = slice(h, h + 1)
+        t0 = time.perf_counter()
+        orc.backward(tensors["q"][:, sl], tensors["k"][:, g:g + 1], tensors["v"][:, g:g + 1], evict_at,
+                     wl.softmax_scale, tensors["do"][:, sl], cu_seqlens=cu)
+        dt += time.perf_counter() - t0
+        heads += 1
+    flops = 14 * wl.D * heads * per_head
     try:
         from threadpoolctl import threadpool_info
 
@@ -269,7 +273,7 @@ def cpu_baseline(wl, tensors, evict_at, heads=2):
     except Exception:  # pragma: no cover
         cores = len(os.sched_getaffinity(0))
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"fp64 forward+backward of q-heads 0..{heads - 1} with KV head 0 over the whole "
+            "sample": f"fp64 forward+backward of q-heads 0..{heads - 1} (each with its KV head) over the whole "
                       f"{wl.name} workload ({flops / 1e12:.3f} visible TFLOP in {dt:.1f} s)"}
 
 
