@@ -82,6 +82,15 @@ def test_varlen_ragged(kvs):
     _parity(kvs, wl, wl.evict_at(), cu=wl.cu_seqlens())
 
 
+def test_varlen_many_short_traces(kvs):
+    """48 packed traces of 1-160 tokens (most shorter than one tile, many
+    tile-straddling offsets): per-trace indexing, tails and tile statistics."""
+    rng = np.random.default_rng(2024)
+    lengths = [int(x) for x in rng.integers(1, 161, 48)]
+    wl = inputs.custom_workload("varlen_many", 6, 3, 64, lengths, 9, 30, 6, "latest_only", varlen=True, seed=17)
+    _parity(kvs, wl, wl.evict_at(), cu=wl.cu_seqlens())
+
+
 # Traces past 8192 rows have key blocks (the prompt) visible to more than two
 # 4096-row chunks: the dK/dV work is then split into row chunks whose fp32
 # partial sums are added afterwards.  Element-by-element parity and bitwise
