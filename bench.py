@@ -14,13 +14,31 @@ time, its algorithmic FLOPs per launch over its average launch duration
 same workload ("cpu_baseline").
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu]
+
+HBM traffic per kernel launch (the ``traffic`` field of the roofline) comes
+from two rocprofv3 counter passes over the benchmark (FETCH_SIZE, then
+WRITE_SIZE; KiB per dispatch), each scaled by what the same counter reads for
+a plain device copy of 1 GiB:
+
+    rocprofv3 --pmc FETCH_SIZE --output-format csv -d OUT/fetch -o run -- python bench.py --no-cpu --no-reprefill --steps 2 --warmup 1
+    rocprofv3 --pmc WRITE_SIZE --output-format csv -d OUT/write -o run -- python bench.py --no-cpu --no-reprefill --steps 2 --warmup 1
+    rocprofv3 --pmc FETCH_SIZE --output-format csv -d OUT/cfetch -o run -- python bench.py --traffic-copy
+    rocprofv3 --pmc WRITE_SIZE --output-format csv -d OUT/cwrite -o run -- python bench.py --traffic-copy
+    python bench.py --traffic-summarize OUT trace16k_gqa4
+
+The summary step writes ``profiles/traffic_<kernel>_<workload>.json`` with a
+hash of the kernel source it was taken on (a later kernel change voids it).
 """
 import argparse
+import csv
+import glob
+import hashlib
 import json
 import math
 import os
 import sys
 import time
+from collections import defaultdict
 
 import numpy as np
 
@@ -43,6 +61,34 @@ def visible_pairs(evict_at, lengths):
     return tot
 
 
+# ---------------------------------------------------------------- HBM traffic from rocprofv3 counters
+COPY_BYTES = 1 << 30
+TRAFFIC_KERNELS = {"fwd_kernel": "fwd", "dkdv_kernel": "bwd_dkdv", "dq_kernel": "bwd_dq", "bwd_pre_kernel": "bwd_pre",
+                   "kstats_kernel": "classify", "paged_decode_kernel": "paged_decode"}
+
+
+def _code_only(text):
+    """Source without // comments, trailing blanks and empty lines: edits to
+    comments do not change the kernels the counters were taken on."""
+    out = []
+    for line in text.splitlines():
+        i = line.find("//")
+        if i >= 0:
+            line = line[:i]
+        line = line.rstrip()
+        if line:
+            out.append(line)
+    return "\n".join(out)
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for f in ("kvs_kernels.hip", "kvs_paged.hip", "kvs_device.h"):
+        with open(os.path.join(ROOT, "paper_2609_35750_amd", "csrc", f), encoding="utf-8") as fh:
+            h.update(_code_only(fh.read()).encode())
+    return h.hexdigest()[:16]
+
+
 def load_traffic(kernel, workload):
     """HBM bytes per launch from the committed counter summary, if it was taken
     on the current kernel source; else None."""
@@ -51,11 +97,75 @@ def load_traffic(kernel, workload):
         return None
     with open(path) as fh:
         rec = json.load(fh)
-    from paper_2609_35750_amd.traffic import kernel_source_hash
-
-    if rec.get("source_hash") != kernel_source_hash(ROOT):
+    if rec.get("source_hash") != kernel_source_hash():
         return None
     return rec.get("bytes_per_launch")
+
+
+def traffic_copy():
+    """The calibration run: a plain device copy of COPY_BYTES, three times."""
+    import torch
+
+    src = torch.empty(COPY_BYTES // 2, dtype=torch.bfloat16, device="cuda:0").fill_(1.0)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": COPY_BYTES}))
+
+
+def _counter_per_kernel(d, counter):
+    vals = defaultdict(list)
+    for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        with open(f) as fh:
+            for r in csv.DictReader(fh):
+                if r["Counter_Name"] == counter:
+                    vals[r["Kernel_Name"]].append(float(r["Counter_Value"]) * 1024.0)   # KiB -> bytes
+    return vals
+
+
+def traffic_summarize(out, workload):
+    """Scaled FETCH/WRITE bytes per launch of each library kernel; writes
+    profiles/traffic_<kernel>_<workload>.json and prints a markdown table."""
+    fetch = _counter_per_kernel(os.path.join(out, "fetch"), "FETCH_SIZE")
+    write = _counter_per_kernel(os.path.join(out, "write"), "WRITE_SIZE")
+    cf = _counter_per_kernel(os.path.join(out, "cfetch"), "FETCH_SIZE")
+    cw = _counter_per_kernel(os.path.join(out, "cwrite"), "WRITE_SIZE")
+    biggest = lambda vals: max((sum(v) / len(v) for v in vals.values()), default=0.0)   # the copy dispatch
+    f_scale, w_scale = COPY_BYTES / biggest(cf), COPY_BYTES / biggest(cw)
+    lines = ["| kernel | FETCH_SIZE (MB/launch, scaled) | WRITE_SIZE (MB/launch, scaled) | launches |", "|---|---|---|---|"]
+    src_hash = kernel_source_hash()
+    for kname, vals in sorted(fetch.items()):
+        short = next((v for k, v in TRAFFIC_KERNELS.items() if k in kname), None)
+        if short is None:
+            continue
+        fb = sum(vals) / len(vals) * f_scale
+        wv = write.get(kname, [0.0])
+        wb = sum(wv) / len(wv) * w_scale
+        lines.append(f"| `{kname.split('(')[0]}` | {fb / 1e6:.1f} | {wb / 1e6:.1f} | {len(vals)} |")
+        rec = {"kernel": short, "workload": workload, "fetch_bytes_per_launch": fb, "write_bytes_per_launch": wb,
+               "bytes_per_launch": fb + wb, "fetch_scale": f_scale, "write_scale": w_scale, "source_hash": src_hash}
+        with open(os.path.join(ROOT, "profiles", f"traffic_{short}_{workload}.json"), "w") as fh:
+            json.dump(rec, fh, indent=1)
+    print(f"copy calibration: FETCH_SIZE x{f_scale:.4f}, WRITE_SIZE x{w_scale:.4f} (copy of {COPY_BYTES} bytes)")
+    print("\n".join(lines))
+
+
+# The paper's own end-to-end numbers, for context only (Abstract; Section 1;
+# Section 5.2; the hardware of Section 4 and the training-details table).
+PAPER_CONTEXT = {
+    "kind": "context, not a target: end-to-end RL training wall-clock (generation + trainer forward/backward) "
+            "of KV-streams over re-prefill compaction, on the paper's hardware; reprefill.time_ratio below is "
+            "the attention-kernel analogue on one MI355X",
+    "claims": [
+        {"speedup": "2.6x to 5x training wall-clock, three compaction strategies", "where": "Abstract"},
+        {"speedup": "5x on TextWorld, 1.3x on ALFWorld", "where": "Section 1"},
+        {"speedup": "3x to peak (Sliding Window, KV-streams vs full context) on SWE", "where": "Section 5.2"},
+    ],
+    "hardware": {"TextWorld": "one 8-GPU H100 node (4 inference, 4 trainer)",
+                 "ALFWorld": "4 A100 GPUs (1 inference, 3 trainer)",
+                 "SWE": "one 8-GPU GB200 node (4 inference, 4 trainer)"},
+}
 
 
 def reprefill_batch(wl):
@@ -288,7 +398,16 @@ def main():
     ap.add_argument("--no-decode", action="store_true", help="skip the paged-cache decode measurement")
     ap.add_argument("--cp-shards", type=int, default=0,
                     help="also time the trace cut into this many context-parallel shards (one after another)")
+    ap.add_argument("--traffic-copy", action="store_true", help="run the 1 GiB copy that calibrates the counters")
+    ap.add_argument("--traffic-summarize", nargs=2, metavar=("OUT", "WORKLOAD"),
+                    help="summarise FETCH/WRITE counter runs under OUT into profiles/")
     args = ap.parse_args()
+    if args.traffic_summarize:
+        traffic_summarize(*args.traffic_summarize)
+        return
+    if args.traffic_copy:
+        traffic_copy()
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the library has no multi-GPU path (--cp-shards N times the "
               "context-parallel shards of the trace one after another on one GPU); run with --gpus 1", file=sys.stderr)
@@ -394,6 +513,7 @@ def main():
     roofline["frac_of_measured_peak"] = achieved / measured_peak
     if not args.no_reprefill:
         out["reprefill"] = reprefill_compare(wl, kvs, args.warmup, args.steps, ms_per_step)
+    out["paper_context"] = PAPER_CONTEXT
     if args.cp_shards > 0 and not wl.varlen:
         out["cp_shards"] = cp_shard_bench(wl, tensors, e, args.cp_shards, args.warmup, args.steps, ms_per_step)
     if not args.no_decode:

@@ -24,7 +24,9 @@
  *  - Tensor pointers are DEVICE pointers owned by the caller; the library
  *    never allocates device memory and keeps no per-call state.  Scratch space
  *    comes from the caller's workspace (size from the *_workspace query; any
- *    256-byte aligned device buffer of at least that size).
+ *    256-byte aligned device buffer of at least that size).  The only
+ *    process-wide state is that of kvs_check_evict_at (calls are serialised)
+ *    and of the benchmark timers kvs_prof_* (see there).
  *  - bf16 tensors are row-major with D innermost:
  *       fixed length:  Q, O, dO, dQ [B][T][Hq][D];  K, V, dK, dV [B][T][Hkv][D]
  *       varlen:        Q, O, dO, dQ [Ntot][Hq][D];  K, V, dK, dV [Ntot][Hkv][D]
@@ -34,6 +36,11 @@
  *  - cu_seqlens (varlen) is a device int32 array [B+1]: cu[0] = 0,
  *    cu[B] = Ntot, non-decreasing; trace b is tokens [cu[b], cu[b+1]).
  *    No attention crosses traces.  max_seqlen must be >= every trace length.
+ *    The host cannot see these offsets, so the kernels never trust them for
+ *    addressing: each trace start is clamped to [0, Ntot], its end to
+ *    [start, Ntot] and its length to max_seqlen.  A malformed cu_seqlens (or a
+ *    trace longer than max_seqlen) gives unspecified results but no access
+ *    outside the caller's buffers; kvs_check_evict_at reports it.
  *  - `stream` is a hipStream_t (NULL = the null stream).  Calls only enqueue
  *    work on it and return; none synchronizes except kvs_check_evict_at.
  *  - Outputs are overwritten, never accumulated.
@@ -55,7 +62,7 @@
 extern "C" {
 #endif
 
-#define KVS_ABI_VERSION 2
+#define KVS_ABI_VERSION 3
 
 typedef enum {
   KVS_OK = 0,
@@ -124,6 +131,43 @@ kvs_status_t kvs_evict_attn_varlen_bwd(const void* dO, const void* Q, const void
                                        float softmax_scale,
                                        void* workspace, size_t workspace_bytes, void* stream);
 
+/* ---------------------------------------------------------------- consistency switches
+ * The forward and backward skip EMPTY tiles and evaluate no mask on FULL
+ * tiles.  These switches turn the shortcuts off without changing anything
+ * else (same kernels, same tile order, same row and key ranges), so that a
+ * caller can check that the shortcuts are exact: the mask must block the
+ * whole deleted span (Section 2, "KV-streams"), so a skipped tile holds no
+ * visible entry and a FULL tile no masked one, and every output (O, LSE, dQ,
+ * dK, dV) must come out bit-identical with and without them.  They cost
+ * time and are meant for tests.
+ *   KVS_FLAG_NO_EMPTY_SKIP    process every key tile of the range a row
+ *                             block walks (and every row block of the range a
+ *                             key block walks), masking the EMPTY ones
+ *   KVS_FLAG_FULL_AS_PARTIAL  evaluate the per-element mask on FULL tiles
+ *
+ * kvs_evict_attn_{fwd,bwd}_ex take either layout: cu_seqlens NULL means B
+ * fixed-length traces of max_seqlen tokens (Ntot must be B * max_seqlen; the
+ * fixed-length layouts above), otherwise the varlen layouts.  Workspace: the
+ * size the matching non-_ex query gives.  Unknown flag bits give
+ * KVS_ERR_UNSUPPORTED; flags = 0 is the plain call.
+ */
+#define KVS_FLAG_NO_EMPTY_SKIP 1u
+#define KVS_FLAG_FULL_AS_PARTIAL 2u
+
+kvs_status_t kvs_evict_attn_fwd_ex(const void* Q, const void* K, const void* V,
+                                   const int32_t* evict_at, const int32_t* cu_seqlens,
+                                   void* O, float* LSE,
+                                   int B, int Ntot, int max_seqlen, int Hq, int Hkv, int D,
+                                   float softmax_scale, unsigned flags,
+                                   void* workspace, size_t workspace_bytes, void* stream);
+kvs_status_t kvs_evict_attn_bwd_ex(const void* dO, const void* Q, const void* K, const void* V,
+                                   const void* O, const float* LSE,
+                                   const int32_t* evict_at, const int32_t* cu_seqlens,
+                                   void* dQ, void* dK, void* dV,
+                                   int B, int Ntot, int max_seqlen, int Hq, int Hkv, int D,
+                                   float softmax_scale, unsigned flags,
+                                   void* workspace, size_t workspace_bytes, void* stream);
+
 /* ---------------------------------------------------------------- tile classes
  * Class of every BM x BN tile of the mask: 0 = EMPTY (no visible element,
  * skipped), 1 = PARTIAL (per-element mask), 2 = FULL (every element
@@ -144,8 +188,11 @@ size_t kvs_classify_tiles_size(const int32_t* lengths, int B, int BM, int BN);
 /* ---------------------------------------------------------------- validation
  * Synchronous check that every key is visible to itself (evict_at[j] > j,
  * trace-local).  On return *first_bad (host) is the packed index of the first
- * offending key, or -1.  Returns KVS_ERR_EVICT if one exists.  cu_seqlens as
- * in kvs_classify_tiles.  Blocks until the stream reaches it.
+ * offending key, or -1.  Returns KVS_ERR_EVICT if one exists, KVS_ERR_SHAPE if
+ * cu_seqlens is not 0 = cu[0] <= ... <= cu[B] = T.  cu_seqlens as in
+ * kvs_classify_tiles.  Blocks until the stream reaches it.  The result passes
+ * through device globals of the library, one copy per GPU, so calls are
+ * serialised within a process (thread-safe; concurrent calls wait).
  */
 kvs_status_t kvs_check_evict_at(const int32_t* evict_at, const int32_t* cu_seqlens, int B, int T,
                                 int64_t* first_bad, void* stream);
@@ -155,8 +202,10 @@ kvs_status_t kvs_check_evict_at(const int32_t* evict_at, const int32_t* cu_seqle
  * kernel it launches with HIP events on the call's stream.  kvs_prof_read
  * waits for the recorded events and returns, for the kernel named `name`
  * ("classify", "fwd", "bwd_pre", "bwd_dkdv", "bwd_dq", "paged_decode"), the
- * number of launches and their total duration in milliseconds.  Not thread-safe;
- * meant for single-threaded benchmark drivers.
+ * number of launches and their total duration in milliseconds.  The records
+ * are process-wide (every thread's launches land in one list, guarded by a
+ * lock), so enable timing only while the calls to be timed are the only
+ * ones running; meant for benchmark drivers.
  */
 void kvs_prof_enable(int on);
 void kvs_prof_reset(void);

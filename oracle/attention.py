@@ -186,3 +186,51 @@ def visible_pairs(evict_at, lengths) -> int:
             tot += int(visible_mask(e[off:off + L], L, i0, i1, i1).sum())
         off += L
     return tot
+
+
+def dq_rounding_scale(q, k, v, evict_at, scale, do, rows, cu_seqlens=None):
+    """Sensitivity of dQ to the two roundings every bf16 backward makes before its dQ sum.
+
+    A backward that receives O in bf16 forms ``Delta_i`` from the rounded O, and
+    a bf16 matrix-core product rounds every ``dS_ij`` to bf16 before
+    ``dQ_i = scale sum_j dS_ij k_j``.  A relative error of at most u in each
+    ``O_id`` and in each ``dS_ij`` moves ``dQ_id`` by at most ``u`` times
+
+        E_id = scale * ( sum_j |dS_ij| |k_jd|  +  |sum_j P_ij k_jd| * sum_d' |dO_id'| |O_id'| )
+
+    (first order; the second term through ``dS_ij = P_ij (dP_ij - Delta_i)``).
+    Returns ``E`` (fp64) for the packed query rows ``rows``: shape
+    ``[len(rows), Hq, D]``.  Test infrastructure for tolerances: P, dS and O
+    are the exact quantities of the definition above, row by row.
+    """
+    q, k, v, do = _f64(q), _f64(k), _f64(v), _f64(do)
+    e = np.asarray(evict_at, dtype=np.int64)
+    rows = np.asarray(rows, dtype=np.int64)
+    n, Hq, D = q.shape
+    G = Hq // k.shape[1]
+    out = np.zeros((rows.size, Hq, D))
+    for a, b in _split(cu_seqlens, n):
+        sel = np.nonzero((rows >= a) & (rows < b))[0]
+        if sel.size == 0:
+            continue
+        L = b - a
+        for c0 in range(0, sel.size, ROW_BLOCK):
+            idx = sel[c0:c0 + ROW_BLOCK]
+            il = rows[idx] - a                       # trace-local rows of this block
+            j1 = int(il.max()) + 1
+            ej = np.minimum(e[a:a + j1], L)[None, :]
+            jj = np.arange(j1)[None, :]
+            M = (jj <= il[:, None]) & (il[:, None] < ej)
+            for h in range(Hq):
+                g = h // G
+                S = np.where(M, scale * (q[a + il, h, :] @ k[a:a + j1, g, :].T), -np.inf)
+                E = np.where(M, np.exp(S - S.max(axis=1, keepdims=True)), 0.0)
+                P = E / E.sum(axis=1, keepdims=True)
+                dP = do[a + il, h, :] @ v[a:a + j1, g, :].T
+                dlt = (P * dP).sum(axis=1, keepdims=True)
+                dS = P * (dP - dlt)
+                O = P @ v[a:a + j1, g, :]
+                R = (np.abs(do[a + il, h, :]) * np.abs(O)).sum(axis=1, keepdims=True)
+                out[idx, h, :] = scale * (np.abs(dS) @ np.abs(k[a:a + j1, g, :])
+                                          + np.abs(P @ k[a:a + j1, g, :]) * R)
+    return out

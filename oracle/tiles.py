@@ -43,3 +43,35 @@ def tile_classes_packed(evict_at: np.ndarray, lengths, BM: int, BN: int) -> np.n
             parts.append(tile_classes(evict_at[off:off + L], L, BM, BN).ravel())
         off += L
     return np.concatenate(parts) if parts else np.zeros(0, dtype=np.uint8)
+
+
+def tile_counts_by_columns(e: np.ndarray, L: int, BM: int, BN: int):
+    """The same counts as ``tile_counts`` without the L x L matrix: key j is
+    visible to rows ``[j, min(e_j, L))``, so within a row block ``[i0, i1)`` it
+    contributes ``max(0, min(i1, e_j, L) - max(i0, j))`` elements; the counts of
+    a tile are those of its key columns summed.  Memory O(L) for long traces."""
+    e = np.minimum(np.asarray(e, dtype=np.int64), L)
+    nqt, nkt = -(-L // BM), -(-L // BN)
+    j = np.arange(L)
+    out = np.zeros((nqt, nkt), dtype=np.int64)
+    pad = np.zeros(nkt * BN, dtype=np.int64)
+    for qt in range(nqt):
+        i0, i1 = qt * BM, min(qt * BM + BM, L)
+        pad[:L] = np.maximum(np.minimum(i1, e) - np.maximum(i0, j), 0)
+        out[qt] = pad.reshape(nkt, BN).sum(axis=1)
+    return out
+
+
+def class_totals(e: np.ndarray, lengths, BM: int, BN: int):
+    """(EMPTY, FULL, PARTIAL) tile totals and the visible elements inside PARTIAL
+    tiles, over packed traces, from ``tile_counts_by_columns``."""
+    tot = np.zeros(3, dtype=np.int64)
+    vis_partial, off = 0, 0
+    for L in lengths:
+        c = tile_counts_by_columns(e[off:off + L], L, BM, BN)
+        full = c == BM * BN
+        empty = c == 0
+        tot += [int(empty.sum()), int(full.sum()), int((~full & ~empty).sum())]
+        vis_partial += int(c[~full & ~empty].sum())
+        off += L
+    return tuple(int(x) for x in tot), vis_partial

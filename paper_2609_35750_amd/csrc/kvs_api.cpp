@@ -5,9 +5,11 @@
 
 #include <hip/hip_runtime_api.h>
 
+#include <atomic>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -109,33 +111,41 @@ kvs_status_t run_bwd(kvs::Problem& p) {
 }
 
 // ---------------------------------------------------------------- timing records
+// Process-wide and only for benchmark drivers: the records are shared (under
+// g_prof_mu), the open bracket of a launch is per thread.
 struct ProfRec {
   const char* name;
   hipEvent_t a, b;
 };
-bool g_prof = false;
+std::atomic<bool> g_prof{false};
+std::mutex g_prof_mu;
 std::vector<ProfRec> g_recs;
-const char* g_pending = nullptr;
-hipEvent_t g_pending_ev = nullptr;
+thread_local const char* t_pending = nullptr;
+thread_local hipEvent_t t_pending_ev = nullptr;
+
+// kvs_check_evict_at keeps its result in device globals of the library; calls
+// are serialised (each one synchronises its stream before it returns).
+std::mutex g_check_mu;
 
 }  // namespace
 
 namespace kvs {
 void prof_begin(const char* name, hipStream_t s) {
-  if (!g_prof) return;
+  if (!g_prof.load()) return;
   hipEvent_t ev;
   if (hipEventCreate(&ev) != hipSuccess) return;
   (void)hipEventRecord(ev, s);
-  g_pending = name;
-  g_pending_ev = ev;
+  t_pending = name;
+  t_pending_ev = ev;
 }
 void prof_end(hipStream_t s) {
-  if (!g_prof || !g_pending_ev) return;
+  if (!g_prof.load() || !t_pending_ev) return;
   hipEvent_t ev;
   if (hipEventCreate(&ev) != hipSuccess) return;
   (void)hipEventRecord(ev, s);
-  g_recs.push_back({g_pending, g_pending_ev, ev});
-  g_pending_ev = nullptr;
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  g_recs.push_back({t_pending, t_pending_ev, ev});
+  t_pending_ev = nullptr;
 }
 }  // namespace kvs
 
@@ -183,9 +193,12 @@ size_t kvs_evict_attn_varlen_bwd_workspace(int B, int Ntot, int max_seqlen, int 
   return bwd_ws(B, max_seqlen, Ntot, Hq, Hkv, D);
 }
 
+constexpr unsigned kKnownFlags = KVS_FLAG_NO_EMPTY_SKIP | KVS_FLAG_FULL_AS_PARTIAL;
+
 static kvs_status_t fwd_common(const void* Q, const void* K, const void* V, const int32_t* evict_at,
                                const int32_t* cu, void* O, float* LSE, int B, int T, long long ntok, int Hq,
-                               int Hkv, int D, float scale, void* ws, size_t ws_bytes, void* stream) {
+                               int Hkv, int D, float scale, unsigned flags, void* ws, size_t ws_bytes,
+                               void* stream) {
   t_err.clear();
   kvs_status_t st = check_dims(B, T, ntok, Hq, Hkv, D);
   if (st != KVS_OK) return st;
@@ -196,20 +209,21 @@ static kvs_status_t fwd_common(const void* Q, const void* K, const void* V, cons
   REQUIRE_PTR(LSE, "LSE");
   if (!evict_at) return fail(KVS_ERR_NULL, "evict_at is NULL");
   if (!(scale > 0.f) || scale != scale) return fail(KVS_ERR_SHAPE, "softmax_scale must be positive and finite");
+  if (flags & ~kKnownFlags) return fail(KVS_ERR_UNSUPPORTED, "unknown flag bits 0x%x", flags & ~kKnownFlags);
   st = check_ws(ws, ws_bytes, fwd_ws(B, ntok));
   if (st != KVS_OK) return st;
   if (ntok == 0) return KVS_OK;
   kvs::Problem p{};
   p.q = Q; p.k = K; p.v = V; p.evict = evict_at; p.cu = cu; p.o = O; p.lse = LSE;
   p.B = B; p.T = T; p.ntok = (int)ntok; p.Hq = Hq; p.Hkv = Hkv; p.D = D; p.G = Hq / Hkv;
-  p.scale = scale; p.ws = ws; p.stream = (hipStream_t)stream;
+  p.flags = (int)flags; p.scale = scale; p.ws = ws; p.stream = (hipStream_t)stream;
   return run_fwd(p);
 }
 
 static kvs_status_t bwd_common(const void* dO, const void* Q, const void* K, const void* V, const void* O,
                                const float* LSE, const int32_t* evict_at, const int32_t* cu, void* dQ, void* dK,
-                               void* dV, int B, int T, long long ntok, int Hq, int Hkv, int D, float scale, void* ws,
-                               size_t ws_bytes, void* stream) {
+                               void* dV, int B, int T, long long ntok, int Hq, int Hkv, int D, float scale,
+                               unsigned flags, void* ws, size_t ws_bytes, void* stream) {
   t_err.clear();
   kvs_status_t st = check_dims(B, T, ntok, Hq, Hkv, D);
   if (st != KVS_OK) return st;
@@ -224,6 +238,7 @@ static kvs_status_t bwd_common(const void* dO, const void* Q, const void* K, con
   REQUIRE_PTR(dV, "dV");
   if (!evict_at) return fail(KVS_ERR_NULL, "evict_at is NULL");
   if (!(scale > 0.f) || scale != scale) return fail(KVS_ERR_SHAPE, "softmax_scale must be positive and finite");
+  if (flags & ~kKnownFlags) return fail(KVS_ERR_UNSUPPORTED, "unknown flag bits 0x%x", flags & ~kKnownFlags);
   st = check_ws(ws, ws_bytes, bwd_ws(B, T, ntok, Hq, Hkv, D));
   if (st != KVS_OK) return st;
   if (ntok == 0) return KVS_OK;
@@ -231,14 +246,14 @@ static kvs_status_t bwd_common(const void* dO, const void* Q, const void* K, con
   p.q = Q; p.k = K; p.v = V; p.o_in = O; p.dout = dO; p.lse_in = LSE; p.evict = evict_at; p.cu = cu;
   p.dq = dQ; p.dk = dK; p.dv = dV;
   p.B = B; p.T = T; p.ntok = (int)ntok; p.Hq = Hq; p.Hkv = Hkv; p.D = D; p.G = Hq / Hkv;
-  p.scale = scale; p.ws = ws; p.stream = (hipStream_t)stream;
+  p.flags = (int)flags; p.scale = scale; p.ws = ws; p.stream = (hipStream_t)stream;
   return run_bwd(p);
 }
 
 kvs_status_t kvs_evict_attn_fwd(const void* Q, const void* K, const void* V, const int32_t* evict_at, void* O,
                                 float* LSE, int B, int T, int Hq, int Hkv, int D, float softmax_scale,
                                 void* workspace, size_t workspace_bytes, void* stream) {
-  return fwd_common(Q, K, V, evict_at, nullptr, O, LSE, B, T, (long long)B * T, Hq, Hkv, D, softmax_scale,
+  return fwd_common(Q, K, V, evict_at, nullptr, O, LSE, B, T, (long long)B * T, Hq, Hkv, D, softmax_scale, 0u,
                     workspace, workspace_bytes, stream);
 }
 
@@ -247,7 +262,7 @@ kvs_status_t kvs_evict_attn_bwd(const void* dO, const void* Q, const void* K, co
                                 int T, int Hq, int Hkv, int D, float softmax_scale, void* workspace,
                                 size_t workspace_bytes, void* stream) {
   return bwd_common(dO, Q, K, V, O, LSE, evict_at, nullptr, dQ, dK, dV, B, T, (long long)B * T, Hq, Hkv, D,
-                    softmax_scale, workspace, workspace_bytes, stream);
+                    softmax_scale, 0u, workspace, workspace_bytes, stream);
 }
 
 kvs_status_t kvs_evict_attn_varlen_fwd(const void* Q, const void* K, const void* V, const int32_t* evict_at,
@@ -255,7 +270,7 @@ kvs_status_t kvs_evict_attn_varlen_fwd(const void* Q, const void* K, const void*
                                        int max_seqlen, int Hq, int Hkv, int D, float softmax_scale, void* workspace,
                                        size_t workspace_bytes, void* stream) {
   if (!cu_seqlens) return fail(KVS_ERR_NULL, "cu_seqlens is NULL");
-  return fwd_common(Q, K, V, evict_at, cu_seqlens, O, LSE, B, max_seqlen, Ntot, Hq, Hkv, D, softmax_scale,
+  return fwd_common(Q, K, V, evict_at, cu_seqlens, O, LSE, B, max_seqlen, Ntot, Hq, Hkv, D, softmax_scale, 0u,
                     workspace, workspace_bytes, stream);
 }
 
@@ -266,7 +281,37 @@ kvs_status_t kvs_evict_attn_varlen_bwd(const void* dO, const void* Q, const void
                                        void* stream) {
   if (!cu_seqlens) return fail(KVS_ERR_NULL, "cu_seqlens is NULL");
   return bwd_common(dO, Q, K, V, O, LSE, evict_at, cu_seqlens, dQ, dK, dV, B, max_seqlen, Ntot, Hq, Hkv, D,
-                    softmax_scale, workspace, workspace_bytes, stream);
+                    softmax_scale, 0u, workspace, workspace_bytes, stream);
+}
+
+// Fixed length (cu_seqlens NULL: B traces of max_seqlen tokens, Ntot = B * max_seqlen) or varlen, with
+// the tile-classifier switches.
+static kvs_status_t ex_dims(const int32_t* cu, int B, int Ntot, int max_seqlen) {
+  if (!cu && (long long)B * max_seqlen != (long long)Ntot)
+    return fail(KVS_ERR_SHAPE, "without cu_seqlens, Ntot (%d) must equal B * max_seqlen (%d * %d)", Ntot, B,
+                max_seqlen);
+  return KVS_OK;
+}
+
+kvs_status_t kvs_evict_attn_fwd_ex(const void* Q, const void* K, const void* V, const int32_t* evict_at,
+                                   const int32_t* cu_seqlens, void* O, float* LSE, int B, int Ntot, int max_seqlen,
+                                   int Hq, int Hkv, int D, float softmax_scale, unsigned flags, void* workspace,
+                                   size_t workspace_bytes, void* stream) {
+  t_err.clear();
+  if (kvs_status_t st = ex_dims(cu_seqlens, B, Ntot, max_seqlen)) return st;
+  return fwd_common(Q, K, V, evict_at, cu_seqlens, O, LSE, B, max_seqlen, Ntot, Hq, Hkv, D, softmax_scale, flags,
+                    workspace, workspace_bytes, stream);
+}
+
+kvs_status_t kvs_evict_attn_bwd_ex(const void* dO, const void* Q, const void* K, const void* V, const void* O,
+                                   const float* LSE, const int32_t* evict_at, const int32_t* cu_seqlens, void* dQ,
+                                   void* dK, void* dV, int B, int Ntot, int max_seqlen, int Hq, int Hkv, int D,
+                                   float softmax_scale, unsigned flags, void* workspace, size_t workspace_bytes,
+                                   void* stream) {
+  t_err.clear();
+  if (kvs_status_t st = ex_dims(cu_seqlens, B, Ntot, max_seqlen)) return st;
+  return bwd_common(dO, Q, K, V, O, LSE, evict_at, cu_seqlens, dQ, dK, dV, B, max_seqlen, Ntot, Hq, Hkv, D,
+                    softmax_scale, flags, workspace, workspace_bytes, stream);
 }
 
 kvs_status_t kvs_classify_tiles(const int32_t* evict_at, const int32_t* cu_seqlens, int B, int T, int BM, int BN,
@@ -303,6 +348,7 @@ kvs_status_t kvs_check_evict_at(const int32_t* evict_at, const int32_t* cu_seqle
   const long long ntok = cu_seqlens ? T : (long long)B * T;
   if (ntok > 0x7fffffffll) return fail(KVS_ERR_UNSUPPORTED, "too many tokens");
   int cu_bad = 0;
+  std::lock_guard<std::mutex> lk(g_check_mu);
   hipError_t e = kvs::launch_check(evict_at, cu_seqlens, B, T, (int)ntok, first_bad, &cu_bad, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "evict_at check");
   if (cu_bad) return fail(KVS_ERR_SHAPE, "cu_seqlens is not 0 = cu[0] <= ... <= cu[B] = Ntot");
@@ -318,9 +364,10 @@ kvs_status_t kvs_measure_mfma_rate(double* tflops, void* stream) {
   return KVS_OK;
 }
 
-void kvs_prof_enable(int on) { g_prof = on != 0; }
+void kvs_prof_enable(int on) { g_prof.store(on != 0); }
 
 void kvs_prof_reset(void) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
   for (auto& r : g_recs) {
     (void)hipEventDestroy(r.a);
     (void)hipEventDestroy(r.b);
@@ -333,6 +380,7 @@ kvs_status_t kvs_prof_read(const char* name, int* launches, double* total_ms) {
   if (!name || !launches || !total_ms) return fail(KVS_ERR_NULL, "NULL argument");
   int n = 0;
   double tot = 0.0;
+  std::lock_guard<std::mutex> lk(g_prof_mu);
   for (auto& r : g_recs) {
     if (std::strcmp(r.name, name) != 0) continue;
     hipError_t e = hipEventSynchronize(r.b);

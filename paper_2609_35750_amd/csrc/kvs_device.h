@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "kvs.h"
+
 namespace kvs {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -40,16 +42,36 @@ __device__ __forceinline__ int tile_class(int i0, int i1, int j0, int j1, int L,
   return kPartial;
 }
 
+// Switches of the tile classifier, for internal-consistency checks: an EMPTY
+// tile is processed (masked) instead of skipped; a FULL tile is masked
+// element by element.  Either way every output must stay bit-identical.
+constexpr int kFlagNoEmptySkip = KVS_FLAG_NO_EMPTY_SKIP;
+constexpr int kFlagFullAsPartial = KVS_FLAG_FULL_AS_PARTIAL;
+
+__host__ __device__ __forceinline__ int adjust_class(int c, int flags) {
+  if ((flags & kFlagNoEmptySkip) && c == kEmpty) c = kPartial;
+  if ((flags & kFlagFullAsPartial) && c == kFull) c = kPartial;
+  return c;
+}
+
 struct Trace {
   int tok0;  // first token of the trace in the packed layout
   int L;     // trace length
 };
 
-__device__ __forceinline__ Trace trace_of(const int* cu, int b, int T) {
-  if (cu) {
-    const int a = cu[b];
-    return {a, cu[b + 1] - a};
-  }
+// Trace b of a packed batch.  Offsets read from device memory are clamped, never
+// trusted for addressing: tok0 to [0, ntok], the end to [tok0, ntok], and the
+// length to T (max_seqlen, which sizes every grid), so a malformed cu_seqlens
+// can give wrong results but no access outside the caller's buffers.
+__host__ __device__ __forceinline__ Trace clamp_trace(int a, int z, int ntok, int T) {
+  a = a < 0 ? 0 : (a > ntok ? ntok : a);
+  z = z < a ? a : (z > ntok ? ntok : z);
+  const int L = z - a;
+  return {a, L < T ? L : T};
+}
+
+__device__ __forceinline__ Trace trace_of(const int* cu, int b, int T, int ntok) {
+  if (cu) return clamp_trace(cu[b], cu[b + 1], ntok, T);
   return {b * T, T};
 }
 

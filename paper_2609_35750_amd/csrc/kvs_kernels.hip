@@ -45,6 +45,7 @@ struct RowArgs {
   uint16_t* dq;         // dQ kernel output
   int B, T, Hq, Hkv, G, HG, TC, nhg, nqt, ntok;
   int varlen;
+  int flags;            // kFlagNoEmptySkip | kFlagFullAsPartial (consistency checks; 0 normally)
   float scale_log2;     // softmax_scale * log2(e)
   float scale;
 };
@@ -66,6 +67,7 @@ struct ColArgs {
   int B, T, Hq, Hkv, G, nkt, ntok;
   int capE;             // slots per KV head (0: no splitting)
   int varlen;
+  int flags;            // as in RowArgs
   float scale_log2;
   float scale;
 };
@@ -94,9 +96,9 @@ __device__ __forceinline__ int2 key_tile_stats(const int* __restrict__ evict, co
 
 // One thread per (trace, key tile of BN keys).
 __global__ void __launch_bounds__(64) kstats_kernel(const int* __restrict__ evict, const int* __restrict__ cu,
-                                                    int T, int BN, int2* __restrict__ out) {
+                                                    int T, int ntok, int BN, int2* __restrict__ out) {
   const int kt = blockIdx.x * kWave + threadIdx.x, b = blockIdx.y;
-  const Trace tr = trace_of(cu, b, T);
+  const Trace tr = trace_of(cu, b, T, ntok);
   const int j0 = kt * BN;
   if (j0 >= tr.L) return;
   out[kstat_index(b, tr.tok0, kt, BN)] = key_tile_stats(evict, tr, j0, BN);
@@ -104,16 +106,18 @@ __global__ void __launch_bounds__(64) kstats_kernel(const int* __restrict__ evic
 
 // ---------------------------------------------------------------- tile-class grid
 // One thread per (trace, q-tile, k-tile); grids of all traces concatenated.
+// With cu_seqlens, T is the packed token count (every trace length is clamped
+// to it, so the grids never outgrow what the host sized from the same offsets).
 __global__ void __launch_bounds__(64) classify_kernel(const int* __restrict__ evict, const int* __restrict__ cu,
                                                       int B, int T, int BM, int BN, uint8_t* __restrict__ out) {
   const int kt = blockIdx.x * kWave + threadIdx.x;
   const int qt = blockIdx.y, b = blockIdx.z;
-  const Trace tr = trace_of(cu, b, T);
+  const Trace tr = trace_of(cu, b, T, T);
   const int nq = (tr.L + BM - 1) / BM, nk = (tr.L + BN - 1) / BN;
   if (qt >= nq || kt >= nk) return;
   long long off = 0;
   for (int bb = 0; bb < b; ++bb) {
-    const Trace t2 = trace_of(cu, bb, T);
+    const Trace t2 = trace_of(cu, bb, T, T);
     off += (long long)((t2.L + BM - 1) / BM) * ((t2.L + BN - 1) / BN);
   }
   const int2 st = key_tile_stats(evict, tr, kt * BN, BN);
@@ -139,8 +143,8 @@ __global__ void __launch_bounds__(256) check_kernel(const int* __restrict__ evic
       if ((b == 0 && a != 0) || z < a || (b == B - 1 && z != ntok) || z > ntok) atomicOr(&g_cu_bad, 1);
     }
   }
-  const Trace tr = trace_of(cu, b, T);
-  if (tr.L <= 0 || tr.tok0 < 0 || tr.tok0 + tr.L > ntok) return;
+  const Trace tr = trace_of(cu, b, T, ntok);
+  if (tr.L <= 0) return;
   for (int j = blockIdx.x * blockDim.x + threadIdx.x; j < tr.L; j += gridDim.x * blockDim.x) {
     if (evict[tr.tok0 + j] <= j) atomicMin(&g_first_bad, (unsigned long long)(tr.tok0 + j));
   }
@@ -156,12 +160,12 @@ struct TileWalker {
 };
 
 __device__ __forceinline__ void walker_load(TileWalker& w, const int2* __restrict__ ks, int kidx0, int i0, int i1,
-                                            int L) {
+                                            int L, int flags) {
   const int kt = w.base + (threadIdx.x & 63);
   bool ne = false, fu = false;
   if (kt < w.lim) {
     const int2 st = ks[kidx0 + kt];
-    const int c = tile_class(i0, i1, kt * kKeyTile, kt * kKeyTile + kKeyTile, L, st.x, st.y);
+    const int c = adjust_class(tile_class(i0, i1, kt * kKeyTile, kt * kKeyTile + kKeyTile, L, st.x, st.y), flags);
     ne = c != kEmpty;
     fu = c == kFull;
   }
@@ -170,11 +174,11 @@ __device__ __forceinline__ void walker_load(TileWalker& w, const int2* __restric
 }
 
 __device__ __forceinline__ int walker_next(TileWalker& w, const int2* __restrict__ ks, int kidx0, int i0, int i1,
-                                           int L) {
+                                           int L, int flags) {
   while (w.live == 0ull) {
     w.base += 64;
     if (w.base >= w.lim) return -1;
-    walker_load(w, ks, kidx0, i0, i1, L);
+    walker_load(w, ks, kidx0, i0, i1, L, flags);
   }
   const int bit = __builtin_ctzll(w.live);
   w.live &= w.live - 1ull;
@@ -226,7 +230,7 @@ __device__ __forceinline__ bool row_tile(const RowArgs& a, RowTile& t) {
   t.b = wg % a.B;
   wg /= a.B;
   const int qt = a.nqt - 1 - wg;  // later query tiles see more keys: start them first
-  t.tr = trace_of(a.cu, t.b, a.T);
+  t.tr = trace_of(a.cu, t.b, a.T, a.ntok);
   const int BMt = 32 * a.TC;
   t.i0 = qt * BMt;
   t.i1 = t.i0 + BMt;
@@ -318,8 +322,8 @@ fwd_kernel(RowArgs a) {
 
   const int kidx0 = kstat_index(rt.b, tr.tok0, 0, kKeyTile);
   TileWalker w{0, (min(rt.i1, tr.L) + kKeyTile - 1) / kKeyTile, 0ull, 0ull};
-  walker_load(w, a.kstats, kidx0, rt.i0, rt.i1, tr.L);
-  int kt = __builtin_amdgcn_readfirstlane(walker_next(w, a.kstats, kidx0, rt.i0, rt.i1, tr.L));
+  walker_load(w, a.kstats, kidx0, rt.i0, rt.i1, tr.L, a.flags);
+  int kt = __builtin_amdgcn_readfirstlane(walker_next(w, a.kstats, kidx0, rt.i0, rt.i1, tr.L, a.flags));
   int2 kst = kt >= 0 ? a.kstats[kidx0 + kt] : make_int2(0, 0);
   int sub = 0;
 
@@ -332,13 +336,13 @@ fwd_kernel(RowArgs a) {
     // next 64-key tile once this one is done or its remaining keys lie past the trace end
     // (a staged sub-tile must start inside the trace)
     if (nsub == NSUB || kt * kKeyTile + nsub * BN >= tr.L) {
-      nkt = __builtin_amdgcn_readfirstlane(walker_next(w, a.kstats, kidx0, rt.i0, rt.i1, tr.L));
+      nkt = __builtin_amdgcn_readfirstlane(walker_next(w, a.kstats, kidx0, rt.i0, rt.i1, tr.L, a.flags));
       nsub = 0;
       if (nkt >= 0) nkst = a.kstats[kidx0 + nkt];
     }
     if (nkt >= 0) stage(nK, nV, nE, nkt, nsub);
     const int j0 = kt * kKeyTile + sub * BN;
-    const int cls = tile_class(rt.i0w, rt.i0w + 32, j0, j0 + BN, tr.L, kst.x, kst.y);
+    const int cls = adjust_class(tile_class(rt.i0w, rt.i0w + 32, j0, j0 + BN, tr.L, kst.x, kst.y), a.flags);
     if (cls != kEmpty) {
       f32x16 s[NKB];
 #pragma unroll
@@ -355,9 +359,12 @@ fwd_kernel(RowArgs a) {
       // The reference max of a row only moves when the tile's max exceeds it by
       // more than 8 (log2 units): probabilities are then at most 2^8, exact to
       // rescale later, and the accumulator rescale is skipped for most tiles.
+      // The ballot moves every row of the wave, including rows that have not
+      // seen a visible key yet and see none here (m_run = mx = -inf): their
+      // factor is 1, not exp2(-inf - -inf) = NaN.
       if (__ballot(mx > m_run + 8.f)) {
         const float m_new = fmaxf(m_run, mx);
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);   // 0 on the first visible tile
+        const float alpha = m_new == m_run ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);   // 0 on the first visible tile
         l_run *= alpha;
 #pragma unroll
         for (int d = 0; d < DB; ++d)
@@ -498,21 +505,21 @@ __global__ void __launch_bounds__(512) dq_kernel(RowArgs a) {
 
   const int kidx0 = kstat_index(rt.b, tr.tok0, 0, kKeyTile);
   TileWalker w{0, (min(rt.i1, tr.L) + kKeyTile - 1) / kKeyTile, 0ull, 0ull};
-  walker_load(w, a.kstats, kidx0, rt.i0, rt.i1, tr.L);
-  int kt = __builtin_amdgcn_readfirstlane(walker_next(w, a.kstats, kidx0, rt.i0, rt.i1, tr.L));
+  walker_load(w, a.kstats, kidx0, rt.i0, rt.i1, tr.L, a.flags);
+  int kt = __builtin_amdgcn_readfirstlane(walker_next(w, a.kstats, kidx0, rt.i0, rt.i1, tr.L, a.flags));
   int2 kst = kt >= 0 ? a.kstats[kidx0 + kt] : make_int2(0, 0);
 
   auto body = [&](const uint16_t* cK, const uint16_t* cV, const int* cE, uint16_t* nK, uint16_t* nV, int* nE) {
     // Statistics of the next tile are read before its copy is issued and used one
     // iteration later, so no wait on this iteration's copies is needed for them.
-    const int nkt = __builtin_amdgcn_readfirstlane(walker_next(w, a.kstats, kidx0, rt.i0, rt.i1, tr.L));
+    const int nkt = __builtin_amdgcn_readfirstlane(walker_next(w, a.kstats, kidx0, rt.i0, rt.i1, tr.L, a.flags));
     int2 nkst = make_int2(0, 0);
     if (nkt >= 0) {
       nkst = a.kstats[kidx0 + nkt];
       stage_kv<D>(kvst, nK, nV, nE, a, rt, nkt, wave, nw, lane);
     }
     const int j0 = kt * kKeyTile;
-    const int cls = tile_class(rt.i0w, rt.i0w + 32, j0, j0 + kKeyTile, tr.L, kst.x, kst.y);
+    const int cls = adjust_class(tile_class(rt.i0w, rt.i0w + 32, j0, j0 + kKeyTile, tr.L, kst.x, kst.y), a.flags);
     if (cls != kEmpty) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
@@ -606,7 +613,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
   if (item.x < 0) return;   // unused list entry
   const int b = item.x / a.nkt, kt = item.x % a.nkt, chunk = item.y;
   const int nchunk = a.plan[2 * item.x], slot0 = a.plan[2 * item.x + 1];
-  const Trace tr = trace_of(a.cu, b, a.T);
+  const Trace tr = trace_of(a.cu, b, a.T, a.ntok);
   const int j0 = kt * kColKeys;
   if (j0 >= tr.L) return;
 
@@ -859,8 +866,8 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
   };
   auto dv_step = [&](int step, const uint16_t* cQ, const uint16_t* cO, const float* cL) __attribute__((always_inline)) {
     const int i0 = (qs_lo + step / a.G) * kQStep;
-    const int c0 = tile_class(i0, i0 + 32, jw0, jw0 + 32, tr.L, emin_w, emax_w);
-    const int c1 = tile_class(i0 + 32, i0 + 64, jw0, jw0 + 32, tr.L, emin_w, emax_w);
+    const int c0 = adjust_class(tile_class(i0, i0 + 32, jw0, jw0 + 32, tr.L, emin_w, emax_w), a.flags);
+    const int c1 = adjust_class(tile_class(i0 + 32, i0 + 64, jw0, jw0 + 32, tr.L, emin_w, emax_w), a.flags);
     if (c0 == kFull && c1 == kFull) {
       dv_full(step, cQ, cO, cL);
     } else {
@@ -884,8 +891,8 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
   };
   auto dk_step = [&](int step, const uint16_t* cQ, const uint16_t* cO, const float* cD) __attribute__((always_inline)) {
     const int i0 = (qs_lo + step / a.G) * kQStep;
-    const int c0 = tile_class(i0, i0 + 32, jw0, jw0 + 32, tr.L, emin_w, emax_w);
-    const int c1 = tile_class(i0 + 32, i0 + 64, jw0, jw0 + 32, tr.L, emin_w, emax_w);
+    const int c0 = adjust_class(tile_class(i0, i0 + 32, jw0, jw0 + 32, tr.L, emin_w, emax_w), a.flags);
+    const int c1 = adjust_class(tile_class(i0 + 32, i0 + 64, jw0, jw0 + 32, tr.L, emin_w, emax_w), a.flags);
     if (c0 != kEmpty && c1 != kEmpty) {
       dk_full(step, cQ, cO, cD);
     } else {
@@ -968,8 +975,8 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
 // items start first.  One workgroup of 1024 threads; block spans come from the
 // 64-key tile statistics.
 __global__ void __launch_bounds__(1024) split_plan_kernel(const int2* __restrict__ kstats, const int* __restrict__ cu,
-                                                          int B, int T, int nkt, int capE, int* __restrict__ plan,
-                                                          int2* __restrict__ items) {
+                                                          int B, int T, int ntok, int nkt, int capE,
+                                                          int* __restrict__ plan, int2* __restrict__ items) {
   constexpr int NBK = 2048;   // sort buckets: row-step counts 0 .. 2047 (longer ones share the last bucket)
   __shared__ int scan[1024];
   __shared__ int bucket[NBK];
@@ -981,7 +988,7 @@ __global__ void __launch_bounds__(1024) split_plan_kernel(const int2* __restrict
   const int b0 = min(tid * per, nblocks), b1 = min(b0 + per, nblocks);
   auto span_of = [&](int blk) {   // query row-steps [j0/64, ceil(emax/64)) of the block; 0 past the trace
     const int b = blk / nkt, kt = blk % nkt;
-    const Trace tr = trace_of(cu, b, T);
+    const Trace tr = trace_of(cu, b, T, ntok);
     const int j0 = kt * kColKeys;
     if (j0 >= tr.L) return 0;
     const int t0 = j0 / kKeyTile, nt = (tr.L + kKeyTile - 1) / kKeyTile;
@@ -1052,14 +1059,14 @@ constexpr int kReduceSplit = 8;
 template <int D>
 __global__ void __launch_bounds__(256) split_reduce_kernel(const int* __restrict__ plan, const float* __restrict__ part,
                                                            const int* __restrict__ cu, uint16_t* __restrict__ dk,
-                                                           uint16_t* __restrict__ dv, int B, int T, int nkt, int Hkv,
-                                                           float scale) {
+                                                           uint16_t* __restrict__ dv, int B, int T, int ntok,
+                                                           int nkt, int Hkv, float scale) {
   const int sub = blockIdx.x % kReduceSplit, wg = blockIdx.x / kReduceSplit;
   const int g = wg % Hkv, blk = wg / Hkv;
   const int nc = plan[2 * blk], s0 = plan[2 * blk + 1];
   if (nc <= 1) return;
   const int b = blk / nkt, kt = blk % nkt;
-  const Trace tr = trace_of(cu, b, T);
+  const Trace tr = trace_of(cu, b, T, ntok);
   constexpr int PER = kColKeys * D / kReduceSplit / 256;   // elements per thread
   static_assert(PER % 4 == 0 && PER >= 4, "reduce slice must be whole float4s per thread");
   for (int which = 0; which < 2; ++which) {
@@ -1152,9 +1159,9 @@ template __global__ void dq_kernel<128>(RowArgs);
 template __global__ void dkdv_kernel<64>(ColArgs);
 template __global__ void dkdv_kernel<128>(ColArgs);
 template __global__ void split_reduce_kernel<64>(const int*, const float*, const int*, uint16_t*, uint16_t*, int, int,
-                                                 int, int, float);
+                                                 int, int, int, float);
 template __global__ void split_reduce_kernel<128>(const int*, const float*, const int*, uint16_t*, uint16_t*, int, int,
-                                                  int, int, float);
+                                                  int, int, int, float);
 
 // ---------------------------------------------------------------- launchers
 size_t ws_kstats_bytes(int B, int ntok) {
@@ -1211,6 +1218,7 @@ static RowArgs row_args(const Problem& p, const int2* kstats) {
   a.nqt = (p.T + 32 * p.TC - 1) / (32 * p.TC);
   a.ntok = p.ntok;
   a.varlen = p.cu != nullptr;
+  a.flags = p.flags;
   a.scale = p.scale;
   a.scale_log2 = p.scale * 1.4426950408889634f;
   return a;
@@ -1219,7 +1227,7 @@ static RowArgs row_args(const Problem& p, const int2* kstats) {
 hipError_t launch_kstats(const Problem& p, int BN, int2* kstats) {
   dim3 grid(((p.T + BN - 1) / BN + kWave - 1) / kWave, p.B);
   prof_begin("classify", p.stream);
-  hipLaunchKernelGGL(kstats_kernel, grid, dim3(kWave), 0, p.stream, p.evict, p.cu, p.T, BN, kstats);
+  hipLaunchKernelGGL(kstats_kernel, grid, dim3(kWave), 0, p.stream, p.evict, p.cu, p.T, p.ntok, BN, kstats);
   prof_end(p.stream);
   return hipGetLastError();
 }
@@ -1270,6 +1278,7 @@ hipError_t launch_bwd_dkdv(const Problem& p, const int2* kstats, const float* de
   a.nkt = (p.T + kColKeys - 1) / kColKeys;
   a.ntok = p.ntok;
   a.varlen = p.cu != nullptr;
+  a.flags = p.flags;
   a.scale = p.scale;
   a.scale_log2 = p.scale * 1.4426950408889634f;
   a.capE = split_cap(p.B, p.T, p.Hkv);
@@ -1282,8 +1291,8 @@ hipError_t launch_bwd_dkdv(const Problem& p, const int2* kstats, const float* de
     a.plan = plan;
     a.items = items;
     a.part = (float*)w;
-    hipLaunchKernelGGL(split_plan_kernel, dim3(1), dim3(1024), 0, p.stream, kstats, p.cu, p.B, p.T, a.nkt, a.capE,
-                       plan, items);
+    hipLaunchKernelGGL(split_plan_kernel, dim3(1), dim3(1024), 0, p.stream, kstats, p.cu, p.B, p.T, p.ntok, a.nkt,
+                       a.capE, plan, items);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -1297,10 +1306,10 @@ hipError_t launch_bwd_dkdv(const Problem& p, const int2* kstats, const float* de
   const dim3 rgrid((unsigned)((long long)p.B * a.nkt * p.Hkv * kReduceSplit));
   if (p.D == 128)
     hipLaunchKernelGGL(split_reduce_kernel<128>, rgrid, dim3(256), 0, p.stream, a.plan, a.part, p.cu,
-                       (uint16_t*)p.dk, (uint16_t*)p.dv, p.B, p.T, a.nkt, p.Hkv, p.scale);
+                       (uint16_t*)p.dk, (uint16_t*)p.dv, p.B, p.T, p.ntok, a.nkt, p.Hkv, p.scale);
   else
     hipLaunchKernelGGL(split_reduce_kernel<64>, rgrid, dim3(256), 0, p.stream, a.plan, a.part, p.cu,
-                       (uint16_t*)p.dk, (uint16_t*)p.dv, p.B, p.T, a.nkt, p.Hkv, p.scale);
+                       (uint16_t*)p.dk, (uint16_t*)p.dv, p.B, p.T, p.ntok, a.nkt, p.Hkv, p.scale);
   return hipGetLastError();
 }
 

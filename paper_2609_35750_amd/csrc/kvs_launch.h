@@ -27,6 +27,7 @@ struct Problem {
   int ntok;     // total packed tokens
   int Hq, Hkv, D, G;
   int HG, TC, nhg;   // q-heads per workgroup, 32-token chunks per workgroup, head groups per KV head
+  int flags;         // tile-classifier switches (kFlagNoEmptySkip, kFlagFullAsPartial); 0 normally
   float scale;
   void* ws;
   hipStream_t stream;

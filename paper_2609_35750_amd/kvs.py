@@ -39,6 +39,10 @@ SIGNATURES = {
     "kvs_evict_attn_varlen_bwd_workspace": (_Z, [_I, _I, _I, _I, _I, _I]),
     "kvs_evict_attn_varlen_bwd": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
                                        _I, _I, _I, _I, _I, _I, _F, _P, _Z, _P]),
+    "kvs_evict_attn_fwd_ex": (_I, [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _F, ctypes.c_uint,
+                                   _P, _Z, _P]),
+    "kvs_evict_attn_bwd_ex": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                                   _I, _I, _I, _I, _I, _I, _F, ctypes.c_uint, _P, _Z, _P]),
     "kvs_classify_tiles": (_I, [_P, _P, _I, _I, _I, _I, _P, _P]),
     "kvs_classify_tiles_size": (_Z, [ctypes.POINTER(ctypes.c_int32), _I, _I, _I]),
     "kvs_check_evict_at": (_I, [_P, _P, _I, _I, ctypes.POINTER(_L), _P]),
@@ -67,6 +71,8 @@ for _name, (_res, _args) in SIGNATURES.items():
 
 KVS_OK, KVS_ERR_NULL, KVS_ERR_SHAPE, KVS_ERR_ALIGN, KVS_ERR_WORKSPACE, KVS_ERR_EVICT, KVS_ERR_HIP, \
     KVS_ERR_UNSUPPORTED, KVS_ERR_CAPACITY, KVS_ERR_STATE = range(10)
+# tile-classifier switches of the *_ex calls (consistency checks)
+FLAG_NO_EMPTY_SKIP, FLAG_FULL_AS_PARTIAL = 1, 2
 
 
 class KvsError(RuntimeError):
@@ -139,12 +145,13 @@ def _check_shapes(q, k, v, evict_at, cu_seqlens, max_seqlen, check_cu, *like_q):
 
 
 def kvs_evict_attn_fwd(q, k, v, evict_at, softmax_scale=None, cu_seqlens=None, max_seqlen=None,
-                       out=None, lse=None, check_cu=True) -> Tuple[torch.Tensor, torch.Tensor]:
+                       out=None, lse=None, check_cu=True, flags=0) -> Tuple[torch.Tensor, torch.Tensor]:
     """Forward of eviction-masked attention; returns ``(O, LSE)``.
 
     Fixed length: q [B,T,Hq,D], k/v [B,T,Hkv,D], evict_at [B,T] -> LSE [B,Hq,T].
     Varlen (``cu_seqlens`` int32 [B+1] on the GPU, ``max_seqlen`` int): q [Ntot,Hq,D],
     k/v [Ntot,Hkv,D], evict_at [Ntot] -> LSE [Hq,Ntot].
+    Nonzero ``flags`` (FLAG_*) go through ``kvs_evict_attn_fwd_ex``.
     """
     _check_dtypes(evict_at, cu_seqlens, q, k, v)
     B, T, ntok, Hq, Hkv, D = _dims(q, k, cu_seqlens)
@@ -157,7 +164,16 @@ def kvs_evict_attn_fwd(q, k, v, evict_at, softmax_scale=None, cu_seqlens=None, m
         raise ValueError(f"LSE must be float32 {lse_shape}")
     _check_shapes(q, k, v, evict_at, cu_seqlens, max_seqlen, check_cu, out)
     s = _stream(q)
-    if cu_seqlens is None:
+    if flags:
+        mx = T if cu_seqlens is None else max_seqlen
+        if mx is None:
+            raise ValueError("max_seqlen is required with cu_seqlens")
+        nws = (lib.kvs_evict_attn_fwd_workspace(B, T, Hq, Hkv, D) if cu_seqlens is None else
+               lib.kvs_evict_attn_varlen_fwd_workspace(B, ntok, int(mx), Hq, Hkv, D))
+        ws = _workspace(nws, q.device)
+        st = lib.kvs_evict_attn_fwd_ex(_ptr(q), _ptr(k), _ptr(v), _ptr(evict_at), _ptr(cu_seqlens), _ptr(out),
+                                       _ptr(lse), B, ntok, int(mx), Hq, Hkv, D, scale, int(flags), _ptr(ws), nws, s)
+    elif cu_seqlens is None:
         nws = lib.kvs_evict_attn_fwd_workspace(B, T, Hq, Hkv, D)
         ws = _workspace(nws, q.device)
         st = lib.kvs_evict_attn_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(evict_at), _ptr(out), _ptr(lse),
@@ -175,8 +191,10 @@ def kvs_evict_attn_fwd(q, k, v, evict_at, softmax_scale=None, cu_seqlens=None, m
 
 
 def kvs_evict_attn_bwd(do, q, k, v, o, lse, evict_at, softmax_scale=None, cu_seqlens=None, max_seqlen=None,
-                       dq=None, dk=None, dv=None, check_cu=True) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
-    """Backward of eviction-masked attention; returns ``(dQ, dK, dV)`` (bf16)."""
+                       dq=None, dk=None, dv=None, check_cu=True,
+                       flags=0) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
+    """Backward of eviction-masked attention; returns ``(dQ, dK, dV)`` (bf16).
+    Nonzero ``flags`` (FLAG_*) go through ``kvs_evict_attn_bwd_ex``."""
     _check_dtypes(evict_at, cu_seqlens, q, k, v, o, do)
     B, T, ntok, Hq, Hkv, D = _dims(q, k, cu_seqlens)
     scale = 1.0 / math.sqrt(D) if softmax_scale is None else float(softmax_scale)
@@ -190,7 +208,17 @@ def kvs_evict_attn_bwd(do, q, k, v, o, lse, evict_at, softmax_scale=None, cu_seq
     if dk.shape != k.shape or dv.shape != k.shape:
         raise ValueError("dK, dV must have the shape of K")
     s = _stream(q)
-    if cu_seqlens is None:
+    if flags:
+        mx = T if cu_seqlens is None else max_seqlen
+        if mx is None:
+            raise ValueError("max_seqlen is required with cu_seqlens")
+        nws = (lib.kvs_evict_attn_bwd_workspace(B, T, Hq, Hkv, D) if cu_seqlens is None else
+               lib.kvs_evict_attn_varlen_bwd_workspace(B, ntok, int(mx), Hq, Hkv, D))
+        ws = _workspace(nws, q.device)
+        st = lib.kvs_evict_attn_bwd_ex(_ptr(do), _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), _ptr(evict_at),
+                                       _ptr(cu_seqlens), _ptr(dq), _ptr(dk), _ptr(dv), B, ntok, int(mx), Hq, Hkv, D,
+                                       scale, int(flags), _ptr(ws), nws, s)
+    elif cu_seqlens is None:
         nws = lib.kvs_evict_attn_bwd_workspace(B, T, Hq, Hkv, D)
         ws = _workspace(nws, q.device)
         st = lib.kvs_evict_attn_bwd(_ptr(do), _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), _ptr(evict_at),

@@ -3,12 +3,16 @@
     python tests/golden/make_parity_fixtures.py [workload ...]
 
 For each workload the fp64 checker runs forward + backward for the q-heads of
-KV head 0 over the whole workload (every trace, every row), and the script
-stores, as float32:
+the first and the last KV head (0 and Hkv - 1) over the whole workload (every
+trace, every row), and the script stores, as float32:
 
 * O, LSE, dQ of those q-heads at a set of sampled query rows that covers the
   prompt, every kind of segment boundary, summaries and the trace ends;
-* dK, dV of KV head 0 at a set of sampled keys chosen the same way.
+* dK, dV of those KV heads at a set of sampled keys chosen the same way;
+* at the sampled rows, the checker's first-order sensitivity of dQ to the
+  roundings of Delta and dS (``oracle.attention.dq_rounding_scale``), which
+  enters the dQ tolerance;
+* the whole-tensor norm of each of O, dQ, dK, dV per KV head.
 
 Inputs are the seeded synthetic tensors of ``paper_2609_35750_amd.inputs``;
 the GPU test regenerates them and compares the library's outputs at the same
@@ -64,25 +68,40 @@ def make(name):
     e = wl.evict_at()
     G = wl.G
     cu = wl.cu_seqlens() if wl.varlen else None
-    res = orc.backward(t["q"][:, :G], t["k"][:, :1], t["v"][:, :1], e, wl.softmax_scale, t["do"][:, :G],
-                       cu_seqlens=cu)
+    kv_heads = sorted({0, wl.Hkv - 1})
     rng = np.random.default_rng(7)
     rows = sample_positions(wl, rng)
     keys = sample_positions(wl, np.random.default_rng(8))
+    parts = {k: [] for k in ("O", "LSE", "dQ", "E_dQ", "dK", "dV", "norm_O", "norm_dQ", "norm_dK", "norm_dV")}
+    for g in kv_heads:
+        hs = slice(g * G, (g + 1) * G)
+        res = orc.backward(t["q"][:, hs], t["k"][:, g:g + 1], t["v"][:, g:g + 1], e, wl.softmax_scale,
+                           t["do"][:, hs], cu_seqlens=cu)
+        parts["O"].append(res["O"][rows].astype(np.float32))
+        parts["LSE"].append(res["LSE"][:, rows].astype(np.float32))
+        parts["dQ"].append(res["dq"][rows].astype(np.float32))
+        parts["E_dQ"].append(orc.dq_rounding_scale(t["q"][:, hs], t["k"][:, g:g + 1], t["v"][:, g:g + 1], e,
+                                                   wl.softmax_scale, t["do"][:, hs], rows,
+                                                   cu_seqlens=cu).astype(np.float32))
+        parts["dK"].append(res["dk"][keys, 0].astype(np.float32))
+        parts["dV"].append(res["dv"][keys, 0].astype(np.float32))
+        for k, src in (("norm_O", "O"), ("norm_dQ", "dq"), ("norm_dK", "dk"), ("norm_dV", "dv")):
+            parts[k].append(np.linalg.norm(res[src]))
+        print(f"{name}: KV head {g} done at {time.time() - t0:.0f} s", flush=True)
     out = {
         "rows": rows,
         "keys": keys,
-        "heads": np.arange(G),
-        "O": res["O"][rows].astype(np.float32),
-        "LSE": res["LSE"][:, rows].astype(np.float32),
-        "dQ": res["dq"][rows].astype(np.float32),
-        "dK": res["dk"][keys, 0].astype(np.float32),
-        "dV": res["dv"][keys, 0].astype(np.float32),
-        # whole-tensor magnitudes of the group's outputs, for relative checks
-        "norm_O": np.float64(np.linalg.norm(res["O"])),
-        "norm_dQ": np.float64(np.linalg.norm(res["dq"])),
-        "norm_dK": np.float64(np.linalg.norm(res["dk"])),
-        "norm_dV": np.float64(np.linalg.norm(res["dv"])),
+        "kv_heads": np.array(kv_heads, dtype=np.int64),
+        # q-heads (g * G .. g * G + G - 1 for each listed KV head g) along axis 1
+        "O": np.concatenate(parts["O"], axis=1),
+        "LSE": np.concatenate(parts["LSE"], axis=0),
+        "dQ": np.concatenate(parts["dQ"], axis=1),
+        "E_dQ": np.concatenate(parts["E_dQ"], axis=1),
+        # KV heads along axis 1
+        "dK": np.stack(parts["dK"], axis=1),
+        "dV": np.stack(parts["dV"], axis=1),
+        # whole-tensor norms of each listed KV head's outputs, for relative checks
+        **{k: np.array(parts[k], dtype=np.float64) for k in ("norm_O", "norm_dQ", "norm_dK", "norm_dV")},
     }
     path = os.path.join(HERE, f"parity_{name}.npz")
     np.savez_compressed(path, **out)
@@ -90,6 +109,7 @@ def make(name):
 
 
 if __name__ == "__main__":
-    names = sys.argv[1:] or ["trace16k_gqa4", "trace32k_latest", "varlen8_gqa5", "trace64k_last2"]
+    names = sys.argv[1:] or ["trace16k_gqa4", "trace32k_latest", "varlen8_gqa5", "trace64k_last2",
+                             "textworld32k_sliding"]
     for n in names:
         make(n)

@@ -39,7 +39,7 @@ def test_binding_covers_every_symbol(kvs):
 
 
 def test_version_and_strings(kvs):
-    assert kvs.lib.kvs_abi_version() == 2
+    assert kvs.lib.kvs_abi_version() == 3
     for s in range(10):
         assert kvs.lib.kvs_status_string(s)
     assert kvs.lib.kvs_status_string(99) == b"unknown status"
@@ -85,6 +85,26 @@ def test_backward_and_varlen_validation(kvs):
     st = L.kvs_evict_attn_varlen_bwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
                                      2, 100, 60, 4, 3, 64, 0.1, FAKE, 1 << 20, None)
     assert st == kvs.KVS_ERR_SHAPE
+
+
+def test_ex_validation(kvs):
+    """The *_ex calls: the fixed layout needs Ntot = B * max_seqlen, unknown flag bits are refused,
+    and every other check is that of the plain calls."""
+    L = kvs.lib
+    fwd_ex = lambda cu, B, N, T, flags, ws_bytes=1 << 20: L.kvs_evict_attn_fwd_ex(
+        FAKE, FAKE, FAKE, FAKE, cu, FAKE, FAKE, B, N, T, 4, 2, 64, 0.125, flags, FAKE, ws_bytes, None)
+    assert fwd_ex(None, 2, 100, 60, 0) == kvs.KVS_ERR_SHAPE          # 100 != 2 * 60
+    assert fwd_ex(None, 2, 120, 60, 4) == kvs.KVS_ERR_UNSUPPORTED     # unknown bit
+    assert fwd_ex(FAKE, 2, 100, 60, 1 << 31) == kvs.KVS_ERR_UNSUPPORTED
+    assert fwd_ex(None, 2, 120, 60, 3, ws_bytes=8) == kvs.KVS_ERR_WORKSPACE
+    need = L.kvs_evict_attn_bwd_workspace(2, 60, 4, 2, 64)
+    bwd_ex = lambda cu, flags, dq=FAKE, ws_bytes=need: L.kvs_evict_attn_bwd_ex(
+        FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, cu, dq, FAKE, FAKE, 2, 120, 60, 4, 2, 64, 0.125, flags, FAKE,
+        ws_bytes, None)
+    assert bwd_ex(None, 8) == kvs.KVS_ERR_UNSUPPORTED
+    assert bwd_ex(None, 1, dq=None) == kvs.KVS_ERR_NULL
+    assert bwd_ex(None, 2, ws_bytes=need - 1) == kvs.KVS_ERR_WORKSPACE
+    assert kvs.FLAG_NO_EMPTY_SKIP == 1 and kvs.FLAG_FULL_AS_PARTIAL == 2
 
 
 def test_classify_and_check_validation(kvs):

@@ -19,7 +19,7 @@ import torch
 
 from oracle import paged as opg
 from paper_2609_35750_amd import inputs
-from tests.gpu_helpers import LSE_ABS, announce, assert_close, to_f64
+from tests.gpu_helpers import REL_L2, announce, assert_close, assert_flat, assert_lse, to_f64
 
 pytestmark = pytest.mark.gpu
 
@@ -78,8 +78,7 @@ def _check(name, seqs, out, scale):
                 continue
             ro, rl = opg.decode(s["q"][t], s["k"], s["v"], opg.live_set(s["e"], t), scale)
             assert_close(f"{name} t={t} seq={i} O", to_f64(o[i]), ro)
-            assert_close(f"{name} t={t} seq={i} LSE", to_f64(lse[i]), rl, max_abs=LSE_ABS, rel_l2=1e-4,
-                         elementwise=False)
+            assert_lse(f"{name} t={t} seq={i}", to_f64(lse[i]), rl)
 
 
 def _seq(e, Hq, Hkv, D, seed):
@@ -160,8 +159,8 @@ def test_empty_and_single_entry_sequences(pg):
     assert np.all(o[0] == 0) and np.all(np.isneginf(lse[0]))
     assert np.all(o[2] == 0) and np.all(np.isneginf(lse[2]))
     ro, rl = opg.decode(q[1], k1, v1, [0], 0.1)
-    assert_close("single O", o[1], ro, max_abs=4e-3)          # one entry: O = v (bf16-exact up to rounding)
-    assert_close("single LSE", lse[1], rl, max_abs=LSE_ABS, rel_l2=1e-4, elementwise=False)
+    assert_flat("single O", o[1], ro, 4e-3, REL_L2)          # one entry: O = v (bf16-exact up to rounding)
+    assert_lse("single", lse[1], rl)
 
 
 def test_long_cache_many_splits(pg):
@@ -220,4 +219,4 @@ def test_bench_configuration_sampled(pg):
     for sq in checked:
         ro, rl = opg.decode(q[sq], kv[sq][0], kv[sq][1], live, 1.0 / math.sqrt(D))
         assert_close(f"bench-config seq={sq} O", o[sq], ro)
-        assert_close(f"bench-config seq={sq} LSE", lse[sq], rl, max_abs=LSE_ABS, rel_l2=1e-4, elementwise=False)
+        assert_lse(f"bench-config seq={sq}", lse[sq], rl)

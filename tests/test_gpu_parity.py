@@ -10,7 +10,8 @@ import torch
 from oracle import attention as orc
 from oracle import tiles as otiles
 from paper_2609_35750_amd import inputs
-from tests.gpu_helpers import LSE_ABS, announce, assert_close, gpu_fwd_bwd, to_f64
+from tests.gpu_helpers import (announce, assert_close, assert_flat, assert_lse, assert_switches_bitwise,
+                               gpu_fwd_bwd, to_f64)
 
 pytestmark = pytest.mark.gpu
 
@@ -24,18 +25,24 @@ def kvs():
     return k
 
 
-def _parity(kvs, wl, e, cu=None, B=None):
+def _parity(kvs, wl, e, cu=None, B=None, switches=True):
+    """Element by element against the checker; then the tile-classifier
+    switches must leave every output bit-identical."""
     t = inputs.make_tensors(wl)
     scale = wl.softmax_scale
     announce(f"{wl.name} lengths={wl.lengths} Hq={wl.Hq} Hkv={wl.Hkv} D={wl.D} varlen={cu is not None} B={B}")
-    res = gpu_fwd_bwd(kvs, t["q"], t["k"], t["v"], t["do"], e, scale, cu_seqlens=cu,
-                      max_seqlen=max(wl.lengths) if cu is not None else None, B=B)
-    ref = orc.backward(t["q"], t["k"], t["v"], e, scale, t["do"],
-                       cu_seqlens=cu if cu is not None else (np.arange(B + 1) * wl.lengths[0] if B else None))
+    mx = max(wl.lengths) if cu is not None else None
+    res = gpu_fwd_bwd(kvs, t["q"], t["k"], t["v"], t["do"], e, scale, cu_seqlens=cu, max_seqlen=mx, B=B)
+    cu_ref = cu if cu is not None else (np.arange(B + 1) * wl.lengths[0] if B else None)
+    ref = orc.backward(t["q"], t["k"], t["v"], e, scale, t["do"], cu_seqlens=cu_ref)
+    E = orc.dq_rounding_scale(t["q"], t["k"], t["v"], e, scale, t["do"], np.arange(wl.ntok), cu_seqlens=cu_ref)
     out = {}
-    for key, rkey in (("O", "O"), ("dq", "dq"), ("dk", "dk"), ("dv", "dv")):
-        out[key] = assert_close(f"{wl.name}:{key}", to_f64(res[key]), ref[rkey])
-    assert_close(f"{wl.name}:LSE", to_f64(res["LSE"]), ref["LSE"], max_abs=LSE_ABS, rel_l2=1e-4, elementwise=False)
+    for key in ("O", "dq", "dk", "dv"):
+        out[key] = assert_close(f"{wl.name}:{key}", to_f64(res[key]), ref[key], E=E if key == "dq" else None)
+    assert_lse(wl.name, to_f64(res["LSE"]), ref["LSE"])
+    if switches:
+        assert_switches_bitwise(kvs, res, t["q"], t["k"], t["v"], t["do"], e, scale, cu_seqlens=cu, max_seqlen=mx,
+                                B=B, label=wl.name)
     return out
 
 
@@ -54,6 +61,12 @@ LAYOUT_CASES = [
     (641, 6, 2, 128, 64, 128, 32, "last2"),
     (700, 3, 3, 64, 33, 97, 13, "latest_only"),
     (1024, 16, 2, 128, 64, 200, 40, "keep_all"),
+    # no permanent prompt: the first keys are evicted, so rows of a wave that see nothing in a key
+    # tile share it with rows that do (the forward's wave-wide rescale must leave them finite)
+    (1000, 4, 2, 128, 0, 100, 20, "keep_all"),
+    (1000, 4, 2, 64, 0, 100, 20, "latest_only"),
+    (777, 8, 1, 128, 0, 60, 12, "last2"),
+    (520, 6, 3, 64, 0, 37, 5, "keep_all"),
 ]
 
 
@@ -80,6 +93,19 @@ def test_varlen_ragged(kvs):
     wl = inputs.custom_workload("varlen_small", 10, 2, 128, [37, 1, 300, 129, 64], 4, 50, 10, "keep_all",
                                 varlen=True, seed=13)
     _parity(kvs, wl, wl.evict_at(), cu=wl.cu_seqlens())
+
+
+def test_varlen_without_prompt(kvs):
+    wl = inputs.custom_workload("varlen_p0", 8, 2, 128, [300, 1, 700, 129, 64], 0, 50, 10, "latest_only",
+                                varlen=True, seed=14)
+    _parity(kvs, wl, wl.evict_at(), cu=wl.cu_seqlens())
+
+
+@pytest.mark.parametrize("D", [128, 64])
+def test_turn_sliding_window_without_prompt(kvs, D):
+    turns = ("sliding_window", 4, 1, 0, 20, 100, 1, 99 + D)
+    wl = inputs.custom_workload(f"turns_p0_D{D}", 8, 2, D, [900], 0, 0, 0, seed=98 + D, turns=turns)
+    _parity(kvs, wl, wl.evict_at())
 
 
 def test_varlen_many_short_traces(kvs):
@@ -168,11 +194,11 @@ def test_self_only_closed_form(kvs):
     v = t["v"].double().numpy()
     G = Hq // Hkv
     for h in range(Hq):
-        assert_close("O", to_f64(res["O"][:, h]), v[:, h // G], max_abs=1e-6, rel_l2=1e-6, elementwise=False)
+        assert_flat("O", to_f64(res["O"][:, h]), v[:, h // G], max_abs=1e-6, rel_l2=1e-6)
     # dS = P (dP - Delta) vanishes up to the fp32 rounding of two sums of the same products
     assert float(res["dq"].abs().max()) < 1e-4 and float(res["dk"].abs().max()) < 1e-4
     ref_dv = t["do"].double().numpy().reshape(L, Hkv, G, D).sum(2)
-    assert_close("dV", to_f64(res["dv"]), ref_dv, max_abs=2e-2, rel_l2=5e-3)
+    assert_close("dV", to_f64(res["dv"]), ref_dv, rel_l2=5e-3)
 
 
 def test_forward_is_deterministic(kvs):

@@ -18,7 +18,7 @@ import torch
 
 from oracle import attention as orc
 from paper_2609_35750_amd import inputs, shard
-from tests.gpu_helpers import LSE_ABS, announce, assert_close, gpu_fwd_bwd, to_f64
+from tests.gpu_helpers import announce, assert_close, assert_lse, gpu_fwd_bwd, to_f64, ulp_bf16
 
 pytestmark = pytest.mark.gpu
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -37,7 +37,10 @@ def _assemble(kvs, q, k, v, do, plans, scale):
     L, Hq, D = q.shape
     Hkv = k.shape[1]
     out = {"O": np.zeros((L, Hq, D)), "LSE": np.zeros((Hq, L)), "dq": np.zeros((L, Hq, D)),
-           "dk": np.zeros((L, Hkv, D)), "dv": np.zeros((L, Hkv, D))}
+           "dk": np.zeros((L, Hkv, D)), "dv": np.zeros((L, Hkv, D)),
+           # half a bf16 spacing per shard partial added into a key (the partials are bf16 outputs;
+           # a reduce-scatter would add fp32 partials instead)
+           "round_dk": np.zeros((L, Hkv, D)), "round_dv": np.zeros((L, Hkv, D))}
     for p in plans:
         keys = torch.from_numpy(p.keys)
         ql = torch.cat([torch.zeros((p.n_g, Hq, D), dtype=q.dtype), q[p.r0:p.r1]])
@@ -46,8 +49,11 @@ def _assemble(kvs, q, k, v, do, plans, scale):
         out["O"][p.r0:p.r1] = to_f64(r["O"][p.n_g:])
         out["LSE"][:, p.r0:p.r1] = to_f64(r["LSE"][:, p.n_g:])
         out["dq"][p.r0:p.r1] = to_f64(r["dq"][p.n_g:])
-        np.add.at(out["dk"], p.keys, to_f64(r["dk"]))
-        np.add.at(out["dv"], p.keys, to_f64(r["dv"]))
+        dk_s, dv_s = to_f64(r["dk"]), to_f64(r["dv"])
+        np.add.at(out["dk"], p.keys, dk_s)
+        np.add.at(out["dv"], p.keys, dv_s)
+        np.add.at(out["round_dk"], p.keys, 0.5 * ulp_bf16(dk_s))
+        np.add.at(out["round_dv"], p.keys, 0.5 * ulp_bf16(dv_s))
     return out
 
 
@@ -62,9 +68,12 @@ def test_shards_match_the_whole_trace(kvs, strategy, aligned, n):
     plans = shard.plan_trace(e, n, inputs.segment_starts(L, p, w, s) if aligned else None)
     got = _assemble(kvs, q, k, v, do, plans, scale)
     ref = orc.backward(q, k, v, e, scale, do)
-    for key in ("O", "dq", "dk", "dv"):
-        assert_close(f"cp {strategy}:{key}", got[key], ref[key])
-    assert_close(f"cp {strategy}:LSE", got["LSE"], ref["LSE"], max_abs=LSE_ABS, rel_l2=1e-4, elementwise=False)
+    E = orc.dq_rounding_scale(q, k, v, e, scale, do, np.arange(L))
+    assert_close(f"cp {strategy}:O", got["O"], ref["O"])
+    assert_close(f"cp {strategy}:dq", got["dq"], ref["dq"], E=E)
+    assert_close(f"cp {strategy}:dk", got["dk"], ref["dk"], extra=got["round_dk"])
+    assert_close(f"cp {strategy}:dv", got["dv"], ref["dv"], extra=got["round_dv"])
+    assert_lse(f"cp {strategy}", got["LSE"], ref["LSE"])
 
 
 def test_fullsize_64k_eight_shards_sampled(kvs):
@@ -79,10 +88,10 @@ def test_fullsize_64k_eight_shards_sampled(kvs):
     announce(f"cp full-size {name}: 8 shards, gathered keys per shard {[pl.n_g for pl in plans]}")
     t = inputs.make_tensors(wl)
     got = _assemble(kvs, t["q"], t["k"], t["v"], t["do"], plans, wl.softmax_scale)
-    G, rows, keys = wl.G, gold["rows"], gold["keys"]
-    assert_close(f"cp {name}:O", got["O"][rows, :G], gold["O"])
-    assert_close(f"cp {name}:dQ", got["dq"][rows, :G], gold["dQ"].astype(np.float64))
-    assert_close(f"cp {name}:dK", got["dk"][keys, 0], gold["dK"])
-    assert_close(f"cp {name}:dV", got["dv"][keys, 0], gold["dV"])
-    assert_close(f"cp {name}:LSE", got["LSE"][:G][:, rows], gold["LSE"], max_abs=LSE_ABS, rel_l2=1e-4,
-                 elementwise=False)
+    G, rows, keys, kvh = wl.G, gold["rows"], gold["keys"], gold["kv_heads"]
+    heads = np.concatenate([np.arange(g * G, (g + 1) * G) for g in kvh])
+    assert_close(f"cp {name}:O", got["O"][rows][:, heads], gold["O"])
+    assert_close(f"cp {name}:dQ", got["dq"][rows][:, heads], gold["dQ"], E=gold["E_dQ"])
+    assert_close(f"cp {name}:dK", got["dk"][keys][:, kvh], gold["dK"], extra=got["round_dk"][keys][:, kvh])
+    assert_close(f"cp {name}:dV", got["dv"][keys][:, kvh], gold["dV"], extra=got["round_dv"][keys][:, kvh])
+    assert_lse(f"cp {name}", got["LSE"][heads][:, rows], gold["LSE"])

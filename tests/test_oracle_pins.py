@@ -327,3 +327,44 @@ def test_turn_padding_and_markovian_thinker_is_half_stride():
     c = inputs.evict_at_turns(0, [3] * 10, "sliding_window", 4, stride=1)
     np.testing.assert_array_equal(c[:18], np.repeat(np.arange(4, 10) * 3, 3))
     assert np.all(c[18:] == 30)
+
+
+def test_dq_rounding_scale_closed_forms():
+    """dq_rounding_scale against cases with a closed form.
+
+    * Every key visible only to itself (e_j = j + 1): P = I, dS = 0, O_i = v_i and
+      sum_j P_ij k_j = k_i, so E_id = scale |k_id| sum_d' |dO_id'| |v_id'|.
+    * Row 1 of a causal trace sees two keys: dS_10 = -dS_11 = P_10 P_11 (dP_10 - dP_11),
+      so the dS part is scale |dS_10| (|k_0d| + |k_1d|).
+    * The Delta part's sum_j P_ij k_j is attention with the keys as values: the
+      checker's forward with V := K.
+    """
+    rng = np.random.default_rng(5)
+    L, Hq, Hkv, D, scale = 9, 4, 2, 8, 0.37
+    q, k, v, do = (rng.standard_normal(s) for s in [(L, Hq, D), (L, Hkv, D), (L, Hkv, D), (L, Hq, D)])
+    G = Hq // Hkv
+    E = orc.dq_rounding_scale(q, k, v, np.arange(1, L + 1), scale, do, np.arange(L))
+    for h in range(Hq):
+        g = h // G
+        want = scale * np.abs(k[:, g]) * (np.abs(do[:, h]) * np.abs(v[:, g])).sum(axis=1, keepdims=True)
+        np.testing.assert_allclose(E[:, h], want, rtol=1e-12)
+    causal = np.full(L, L)
+    E = orc.dq_rounding_scale(q, k, v, causal, scale, do, np.arange(L))
+    O, _ = orc.forward(q, k, v, causal, scale)
+    B, _ = orc.forward(q, k, k, causal, scale)   # sum_j P_ij k_j
+    for h in range(Hq):
+        g = h // G
+        s0, s1 = scale * q[1, h] @ k[0, g], scale * q[1, h] @ k[1, g]
+        p0 = 1.0 / (1.0 + math.exp(s1 - s0))
+        p1 = 1.0 - p0
+        ds = p0 * p1 * (do[1, h] @ v[0, g] - do[1, h] @ v[1, g])
+        R = (np.abs(do[1, h]) * np.abs(O[1, h])).sum()
+        want = scale * (abs(ds) * (np.abs(k[0, g]) + np.abs(k[1, g])) + np.abs(B[1, h]) * R)
+        np.testing.assert_allclose(E[1, h], want, rtol=1e-10)
+    # rows may be given in any order and subset; varlen traces are independent
+    rows = np.array([7, 2, 5])
+    np.testing.assert_allclose(orc.dq_rounding_scale(q, k, v, causal, scale, do, rows), E[rows], rtol=1e-12)
+    cu = np.array([0, 4, 9])
+    Ev = orc.dq_rounding_scale(q, k, v, np.r_[np.full(4, 4), np.full(5, 5)], scale, do, np.arange(L), cu)
+    np.testing.assert_allclose(Ev[:4], orc.dq_rounding_scale(q[:4], k[:4], v[:4], np.full(4, 4), scale, do[:4],
+                                                             np.arange(4)), rtol=1e-12)
