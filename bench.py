@@ -31,6 +31,7 @@ hash of the kernel source it was taken on (a later kernel change voids it).
 """
 import argparse
 import csv
+import dataclasses
 import glob
 import hashlib
 import json
@@ -398,6 +399,8 @@ def main():
     ap.add_argument("--no-decode", action="store_true", help="skip the paged-cache decode measurement")
     ap.add_argument("--cp-shards", type=int, default=0,
                     help="also time the trace cut into this many context-parallel shards (one after another)")
+    ap.add_argument("--hq", type=int, default=0,
+                    help="diagnostics: override the workload's q-head count (a multiple of its KV heads)")
     ap.add_argument("--traffic-copy", action="store_true", help="run the 1 GiB copy that calibrates the counters")
     ap.add_argument("--traffic-summarize", nargs=2, metavar=("OUT", "WORKLOAD"),
                     help="summarise FETCH/WRITE counter runs under OUT into profiles/")
@@ -418,6 +421,10 @@ def main():
     from paper_2609_35750_amd import inputs, kvs
 
     wl = inputs.WORKLOADS[args.workload]
+    if args.hq:
+        if args.hq % wl.Hkv:
+            sys.exit(f"--hq must be a multiple of the workload's {wl.Hkv} KV heads")
+        wl = dataclasses.replace(wl, Hq=args.hq, name=f"{wl.name}_hq{args.hq}")
     dev = torch.device("cuda:0")
     tensors = inputs.make_tensors(wl)
     e = wl.evict_at()

@@ -221,15 +221,19 @@ struct RowTile {
   Trace tr;
 };
 
+// Launch order: blockIdx % Hkv is the KV head (consecutive workgroups go to
+// different XCDs, so each XCD's L2 serves one head's K/V); then the head
+// group; then the traces one after another, each trace's query tiles from the
+// last to the first (later tiles see more keys: start them first).  Taking
+// the traces one at a time keeps an XCD's K/V working set to one trace.
 __device__ __forceinline__ bool row_tile(const RowArgs& a, RowTile& t) {
   int wg = blockIdx.x;
   t.g = wg % a.Hkv;
   wg /= a.Hkv;
   const int hgrp = wg % a.nhg;
   wg /= a.nhg;
-  t.b = wg % a.B;
-  wg /= a.B;
-  const int qt = a.nqt - 1 - wg;  // later query tiles see more keys: start them first
+  const int qt = a.nqt - 1 - wg % a.nqt;
+  t.b = wg / a.nqt;
   t.tr = trace_of(a.cu, t.b, a.T, a.ntok);
   const int BMt = 32 * a.TC;
   t.i0 = qt * BMt;
@@ -318,7 +322,11 @@ fwd_kernel(RowArgs a) {
   f32x16 acc[DB];
 #pragma unroll
   for (int d = 0; d < DB; ++d) acc[d] = f32x16{};
-  float m_run = -INFINITY, l_run = 0.f;
+  // Running reference maximum of the row (log2 units), the offset the
+  // exponentials use (0 until the row has seen a visible key), and the raw
+  // score above which the reference must move: m_run + 8 in score units.
+  float m_run = -INFINITY, l_run = 0.f, m_use = 0.f, thr = -INFINITY;
+  const float inv_scale_log2 = 1.f / a.scale_log2;
 
   const int kidx0 = kstat_index(rt.b, tr.tok0, 0, kKeyTile);
   TileWalker w{0, (min(rt.i1, tr.L) + kKeyTile - 1) / kKeyTile, 0ull, 0ull};
@@ -350,20 +358,21 @@ fwd_kernel(RowArgs a) {
         s[kb] = scores_t<D, true>(cK, 32 * kb, qreg, rl);
         if (cls == kPartial) mask_t(s[kb], cE, kb, j0, i, tr.L, half);
       }
-      float mx = -INFINITY;
+      float mx = -INFINITY;   // maximum of this lane's half of the row
 #pragma unroll
       for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
-      mx = fmaxf(mx, wave_xor32(mx)) * a.scale_log2;
       // The reference max of a row only moves when the tile's max exceeds it by
       // more than 8 (log2 units): probabilities are then at most 2^8, exact to
       // rescale later, and the accumulator rescale is skipped for most tiles.
-      // The ballot moves every row of the wave, including rows that have not
-      // seen a visible key yet and see none here (m_run = mx = -inf): their
+      // The row's max exceeds the threshold iff one of its two halves does, so
+      // the halves are combined only when some row of the wave moves.  The
+      // ballot moves every row of the wave, including rows that have not seen
+      // a visible key yet and see none here (m_run = row max = -inf): their
       // factor is 1, not exp2(-inf - -inf) = NaN.
-      if (__ballot(mx > m_run + 8.f)) {
-        const float m_new = fmaxf(m_run, mx);
+      if (__ballot(mx > thr)) {
+        const float m_new = fmaxf(m_run, fmaxf(mx, wave_xor32(mx)) * a.scale_log2);
         const float alpha = m_new == m_run ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);   // 0 on the first visible tile
         l_run *= alpha;
 #pragma unroll
@@ -371,8 +380,9 @@ fwd_kernel(RowArgs a) {
 #pragma unroll
           for (int r = 0; r < 16; ++r) acc[d][r] *= alpha;
         m_run = m_new;
+        m_use = (m_run == -INFINITY) ? 0.f : m_run;
+        thr = (m_run + 8.f) * inv_scale_log2;
       }
-      const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
       float ls = 0.f;
 #pragma unroll
       for (int kb = 0; kb < NKB; ++kb)
