@@ -1009,7 +1009,19 @@ __global__ void __launch_bounds__(1024) split_plan_kernel(const int2* __restrict
   auto chunks_of = [](int span) {
     return span > 2 * kSplitRowSteps ? (span + kSplitRowSteps - 1) / kSplitRowSteps : 0;
   };
-  auto key_of = [](int rows) { return min(rows, NBK - 1); };
+  // Sort key (larger first).  One trace (or more than NBK / 8): the row-step
+  // count.  Otherwise the row-step count in classes of Q >= 8 steps, then the
+  // trace, so that items of one trace with about the same length are listed
+  // together and run side by side (they share Q / dO rows in an XCD's L2);
+  // the longest class still starts first, so the tail grows by less than Q
+  // steps.  Keys stay below NBK: nclass * B <= NBK.
+  const bool by_trace = B > 1 && B <= NBK / 8;
+  const int Q = by_trace ? max(8, (NBK + NBK / B - 1) / (NBK / B)) : 1;
+  const int nclass = (NBK + Q - 1) / Q;
+  auto key_of = [&](int rows, int blk) {
+    const int r = min(rows, NBK - 1);
+    return by_trace ? min(r / Q, nclass - 1) * B + blk / nkt : r;
+  };
   int tot = 0;
   for (int blk = b0; blk < b1; ++blk) tot += chunks_of(span_of(blk));
   scan[tid] = tot;
@@ -1029,9 +1041,9 @@ __global__ void __launch_bounds__(1024) split_plan_kernel(const int2* __restrict
     run += w;
     if (span == 0) continue;
     if (grant)
-      for (int c = 0; c < w; ++c) atomicAdd(&bucket[key_of(min(kSplitRowSteps, span - c * kSplitRowSteps))], 1);
+      for (int c = 0; c < w; ++c) atomicAdd(&bucket[key_of(min(kSplitRowSteps, span - c * kSplitRowSteps), blk)], 1);
     else
-      atomicAdd(&bucket[key_of(span)], 1);
+      atomicAdd(&bucket[key_of(span, blk)], 1);
   }
   __syncthreads();
   // bucket start positions, longest first: thread t owns buckets NBK-1-2t and NBK-2-2t
@@ -1055,9 +1067,9 @@ __global__ void __launch_bounds__(1024) split_plan_kernel(const int2* __restrict
     const int nc = plan[2 * blk];
     if (nc > 1) {
       for (int c = 0; c < nc; ++c)
-        items[atomicAdd(&bucket[key_of(min(kSplitRowSteps, span - c * kSplitRowSteps))], 1)] = make_int2(blk, c);
+        items[atomicAdd(&bucket[key_of(min(kSplitRowSteps, span - c * kSplitRowSteps), blk)], 1)] = make_int2(blk, c);
     } else {
-      items[atomicAdd(&bucket[key_of(span)], 1)] = make_int2(blk, 0);
+      items[atomicAdd(&bucket[key_of(span, blk)], 1)] = make_int2(blk, 0);
     }
   }
 }
