@@ -399,6 +399,8 @@ def main():
     ap.add_argument("--no-decode", action="store_true", help="skip the paged-cache decode measurement")
     ap.add_argument("--cp-shards", type=int, default=0,
                     help="also time the trace cut into this many context-parallel shards (one after another)")
+    ap.add_argument("--graph", action="store_true",
+                    help="time replays of one step captured as a HIP graph (no host launch gaps)")
     ap.add_argument("--hq", type=int, default=0,
                     help="diagnostics: override the workload's q-head count (a multiple of its KV heads)")
     ap.add_argument("--traffic-copy", action="store_true", help="run the 1 GiB copy that calibrates the counters")
@@ -455,11 +457,27 @@ def main():
 
     for _ in range(args.warmup):
         step()
+    timed = step
+    if args.graph:
+        # One step (forward call + backward call) captured as a HIP graph and
+        # replayed: the same kernels with the same arguments, without the host
+        # launch gaps between them.
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step()
+        torch.cuda.current_stream().wait_stream(side)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        for _ in range(args.warmup):
+            graph.replay()
+        timed = graph.replay
     # Timed region: exactly K steps, nothing else on the stream.
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        step()
+        timed()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     # The same K steps again with HIP events around every kernel on its launch
@@ -505,6 +523,7 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
+        "launch": "hip_graph" if args.graph else "eager",
         "config": {"workload": wl.name, "traces": wl.B, "tokens": wl.ntok, "Hq": wl.Hq, "Hkv": wl.Hkv, "D": wl.D,
                    "layout": {"prompt": wl.p, "turns": wl.w, "summary": wl.s, "strategy": wl.strategy},
                    "visible_pairs_per_head": vis, "visible_tflop_per_step": (f_fwd + f_bwd) / 1e12},
