@@ -168,6 +168,27 @@ kvs_status_t kvs_evict_attn_bwd_ex(const void* dO, const void* Q, const void* K,
                                    float softmax_scale, unsigned flags,
                                    void* workspace, size_t workspace_bytes, void* stream);
 
+/* ---------------------------------------------------------------- allocation-free forward
+ * For callers that cannot allocate device memory or hand over a workspace:
+ * code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  kvs_evict_attn_fwd_ex (flags 0) without the workspace: the
+ * per-key-tile statistics the forward needs go to a library-owned device
+ * array of 256 KiB, one copy per GPU, held from the first call on that GPU
+ * until the process ends.  Layouts and cu_seqlens as in the *_ex calls.
+ * The call allocates nothing (no hipMalloc, no hipFree, no allocating library
+ * routine).  Limit: B + Ntot / 64 + 2 <= 32768 key tiles (one trace of up to
+ * the 1,048,576-token maximum, or e.g. 8 traces of 110k tokens); beyond it
+ * KVS_ERR_UNSUPPORTED.  Every call on a GPU uses that GPU's one array, which
+ * keeps the last call's contents (each entry a kernel reads is written
+ * earlier in the same call): calls that overlap on one GPU (several streams
+ * or threads) race and give wrong results, so issue them on one stream.
+ */
+kvs_status_t kvs_evict_attn_fwd_noalloc(const void* Q, const void* K, const void* V,
+                                        const int32_t* evict_at, const int32_t* cu_seqlens,
+                                        void* O, float* LSE,
+                                        int B, int Ntot, int max_seqlen, int Hq, int Hkv, int D,
+                                        float softmax_scale, void* stream);
+
 /* ---------------------------------------------------------------- tile classes
  * Class of every BM x BN tile of the mask: 0 = EMPTY (no visible element,
  * skipped), 1 = PARTIAL (per-element mask), 2 = FULL (every element

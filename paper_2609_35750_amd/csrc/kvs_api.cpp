@@ -314,6 +314,33 @@ kvs_status_t kvs_evict_attn_bwd_ex(const void* dO, const void* Q, const void* K,
                     softmax_scale, flags, workspace, workspace_bytes, stream);
 }
 
+kvs_status_t kvs_evict_attn_fwd_noalloc(const void* Q, const void* K, const void* V, const int32_t* evict_at,
+                                        const int32_t* cu_seqlens, void* O, float* LSE, int B, int Ntot,
+                                        int max_seqlen, int Hq, int Hkv, int D, float softmax_scale, void* stream) {
+  t_err.clear();
+  if (kvs_status_t st = ex_dims(cu_seqlens, B, Ntot, max_seqlen)) return st;
+  if (kvs_status_t st = check_dims(B, max_seqlen, Ntot, Hq, Hkv, D)) return st;
+  const size_t need = fwd_ws(B, Ntot);
+  if (need > kvs::kNoAllocScratchBytes)
+    return fail(KVS_ERR_UNSUPPORTED, "allocation-free forward: %zu bytes of scratch needed, %zu available "
+                "(B + Ntot / 64 + 2 must stay within %zu key tiles)", need, kvs::kNoAllocScratchBytes,
+                kvs::kNoAllocScratchBytes / 8);
+  REQUIRE_PTR(Q, "Q");
+  REQUIRE_PTR(K, "K");
+  REQUIRE_PTR(V, "V");
+  REQUIRE_PTR(O, "O");
+  REQUIRE_PTR(LSE, "LSE");
+  if (!evict_at) return fail(KVS_ERR_NULL, "evict_at is NULL");
+  if (!(softmax_scale > 0.f) || softmax_scale != softmax_scale)
+    return fail(KVS_ERR_SHAPE, "softmax_scale must be positive and finite");
+  if (Ntot == 0) return KVS_OK;
+  void* scratch = nullptr;
+  hipError_t e = kvs::noalloc_scratch(&scratch);
+  if (e != hipSuccess) return hip_fail(e, "device address of the library scratch");
+  return fwd_common(Q, K, V, evict_at, cu_seqlens, O, LSE, B, max_seqlen, Ntot, Hq, Hkv, D, softmax_scale, 0u,
+                    scratch, kvs::kNoAllocScratchBytes, stream);
+}
+
 kvs_status_t kvs_classify_tiles(const int32_t* evict_at, const int32_t* cu_seqlens, int B, int T, int BM, int BN,
                                 uint8_t* tile_class, void* stream) {
   t_err.clear();

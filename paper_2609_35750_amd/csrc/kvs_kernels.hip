@@ -25,6 +25,7 @@
 
 #include <algorithm>
 #include <climits>
+#include <mutex>
 #include <type_traits>
 
 namespace kvs {
@@ -1184,6 +1185,32 @@ template __global__ void split_reduce_kernel<64>(const int*, const float*, const
                                                  int, int, int, float);
 template __global__ void split_reduce_kernel<128>(const int*, const float*, const int*, uint16_t*, uint16_t*, int, int,
                                                   int, int, int, float);
+
+// ---------------------------------------------------------------- library-owned scratch (allocation-free forward)
+// Per-key-tile statistics of kvs_evict_attn_fwd_noalloc.  In host code the
+// name `scratch` is only a host-side stand-in: its device address (one per
+// GPU) comes from hipGetSymbolAddress, taken once per device with that device
+// current, and only that address is ever passed to a kernel.
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+hipError_t noalloc_scratch(void** ptr) {
+  static std::mutex mu;
+  static void* per_device[kMaxDevices] = {};
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(mu);
+  if (!per_device[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    per_device[dev] = p;
+  }
+  *ptr = per_device[dev];
+  return hipSuccess;
+}
 
 // ---------------------------------------------------------------- launchers
 size_t ws_kstats_bytes(int B, int ntok) {

@@ -35,6 +35,12 @@ struct Problem {
 
 // Workspace pieces (byte offsets from the workspace start).
 size_t ws_kstats_bytes(int B, int ntok);
+
+// Library-owned scratch of the allocation-free forward: kNoAllocScratchBytes
+// per GPU (device address of this device's copy in *ptr; taken once per device).
+constexpr size_t kNoAllocScratchBytes = 256 * 1024;
+constexpr int kMaxDevices = 64;
+hipError_t noalloc_scratch(void** ptr);
 size_t ws_delta_bytes(int Hq, int ntok);
 size_t ws_split_bytes(int B, int T, int Hkv, int D);
 

@@ -43,6 +43,7 @@ SIGNATURES = {
                                    _P, _Z, _P]),
     "kvs_evict_attn_bwd_ex": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
                                    _I, _I, _I, _I, _I, _I, _F, ctypes.c_uint, _P, _Z, _P]),
+    "kvs_evict_attn_fwd_noalloc": (_I, [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _P]),
     "kvs_classify_tiles": (_I, [_P, _P, _I, _I, _I, _I, _P, _P]),
     "kvs_classify_tiles_size": (_Z, [ctypes.POINTER(ctypes.c_int32), _I, _I, _I]),
     "kvs_check_evict_at": (_I, [_P, _P, _I, _I, ctypes.POINTER(_L), _P]),

@@ -107,6 +107,20 @@ def test_ex_validation(kvs):
     assert kvs.FLAG_NO_EMPTY_SKIP == 1 and kvs.FLAG_FULL_AS_PARTIAL == 2
 
 
+def test_noalloc_forward_validation(kvs):
+    """The allocation-free forward refuses problems beyond its scratch before any HIP call."""
+    L = kvs.lib
+    call = lambda cu, B, N, T, Hq=4, Hkv=2, D=64: L.kvs_evict_attn_fwd_noalloc(
+        FAKE, FAKE, FAKE, FAKE, cu, FAKE, FAKE, B, N, T, Hq, Hkv, D, 0.125, None)
+    # 32768 key tiles of statistics at most: B + Ntot / 64 + 2
+    assert call(FAKE, 4, 2_200_000, 1 << 20) == kvs.KVS_ERR_UNSUPPORTED
+    assert b"scratch" in L.kvs_last_error()
+    assert call(None, 2, 100, 60) == kvs.KVS_ERR_SHAPE          # fixed layout: Ntot = B * max_seqlen
+    assert call(None, 2, 120, 60, Hq=6, Hkv=4) == kvs.KVS_ERR_SHAPE
+    st = L.kvs_evict_attn_fwd_noalloc(None, FAKE, FAKE, FAKE, None, FAKE, FAKE, 2, 120, 60, 4, 2, 64, 0.125, None)
+    assert st == kvs.KVS_ERR_NULL
+
+
 def test_classify_and_check_validation(kvs):
     L = kvs.lib
     assert L.kvs_classify_tiles(FAKE, None, 1, 100, 20, 64, FAKE, None) == kvs.KVS_ERR_SHAPE
