@@ -232,14 +232,6 @@ void kvs_prof_enable(int on);
 void kvs_prof_reset(void);
 kvs_status_t kvs_prof_read(const char* name, int* launches, double* total_ms);
 
-/* Measured dense bf16 MFMA rate of the current device in TFLOP/s (*tflops,
- * host): eight independent chains of v_mfma_f32_32x32x16_bf16 per wave on
- * register operands, four 256-thread workgroups per compute unit, timed with
- * HIP events on `stream` after one warm-up launch.  The attainable peak under
- * the chip's clock at full MFMA load, to report kernel efficiency beside the
- * published peak (256 CU x 2.4 GHz x 4096 FLOP/clk).  Synchronous.  Returns
- * KVS_ERR_NULL for a NULL tflops and KVS_ERR_HIP on a launch or event error. */
-kvs_status_t kvs_measure_mfma_rate(double* tflops, void* stream);
 
 /* ================================================================ streamed paged KV cache
  * The inference side of KV-streams (Section 2, "KV-streams"; Section 4,

@@ -16,6 +16,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libkvs.so")
+# benchmark-only probe of the matrix-core rate (loaded by bench.py, not part of the libkvs ABI)
+BENCH_LIB = os.path.join(HERE, "libkvs_bench.so")
 ARCH = "gfx950"
 
 HIP_FLAGS = [
@@ -33,7 +35,9 @@ def _hipcc() -> str:
 
 
 def build(verbose: bool = False) -> str:
-    """Compile the kernels and the C ABI into ``libkvs.so`` next to this file; returns its path."""
+    """Compile the kernels and the C ABI into ``libkvs.so`` (and the benchmark's
+    matrix-core probe into ``libkvs_bench.so``) next to this file; returns the
+    library's path."""
     hipcc = _hipcc()
     objdir = os.path.join(ROOT, "_build")
     os.makedirs(objdir, exist_ok=True)
@@ -47,6 +51,9 @@ def build(verbose: bool = False) -> str:
     tmp = LIB + ".tmp"
     _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp], verbose)
     os.replace(tmp, LIB)
+    tmp = BENCH_LIB + ".tmp"
+    _run([hipcc, *HIP_FLAGS, "-x", "hip", "-shared", os.path.join(CSRC, "bench_mfma_probe.hip"), "-o", tmp], verbose)
+    os.replace(tmp, BENCH_LIB)
     return LIB
 
 

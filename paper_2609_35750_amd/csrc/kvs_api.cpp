@@ -383,14 +383,6 @@ kvs_status_t kvs_check_evict_at(const int32_t* evict_at, const int32_t* cu_seqle
   return KVS_OK;
 }
 
-kvs_status_t kvs_measure_mfma_rate(double* tflops, void* stream) {
-  t_err.clear();
-  if (!tflops) return fail(KVS_ERR_NULL, "tflops is NULL");
-  hipError_t e = kvs::measure_mfma_rate(tflops, (hipStream_t)stream);
-  if (e != hipSuccess) return hip_fail(e, "MFMA rate probe");
-  return KVS_OK;
-}
-
 void kvs_prof_enable(int on) { g_prof.store(on != 0); }
 
 void kvs_prof_reset(void) {

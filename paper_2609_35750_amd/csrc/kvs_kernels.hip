@@ -1114,66 +1114,6 @@ __global__ void __launch_bounds__(256) split_reduce_kernel(const int* __restrict
   }
 }
 
-// ---------------------------------------------------------------- MFMA rate probe
-// Dense bf16 MFMA throughput of the device, for reporting kernel efficiency
-// against a measured peak as well as the published one: every wave runs
-// eight independent accumulation chains of v_mfma_f32_32x32x16_bf16 on
-// register operands.  The result only feeds a store that never happens, so
-// the products cannot be removed.
-__device__ float g_mfma_sink;
-
-__global__ void __launch_bounds__(256) mfma_rate_kernel(int iters) {
-  const int lane = threadIdx.x & 63;
-  bf16x8 a, b;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    a[e] = (__bf16)(1.0f + 0.001f * (float)((lane + e) & 7));
-    b[e] = (__bf16)(1.0f - 0.001f * (float)((lane * 3 + e) & 7));
-  }
-  f32x16 c[8];
-#pragma unroll
-  for (int k = 0; k < 8; ++k) c[k] = f32x16{};
-  for (int it = 0; it < iters; ++it) {
-#pragma unroll
-    for (int k = 0; k < 8; ++k) c[k] = mfma32(a, b, c[k]);
-  }
-  float s = 0.f;
-#pragma unroll
-  for (int k = 0; k < 8; ++k)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) s += c[k][r];
-  if (s == -1.0f) g_mfma_sink = s;   // never true: the sum is positive
-}
-
-hipError_t measure_mfma_rate(double* tflops, hipStream_t stream) {
-  int dev = 0, ncu = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return e;
-  e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
-  if (e != hipSuccess) return e;
-  const int blocks = 4 * ncu, iters = 4096;
-  hipEvent_t t0, t1;
-  if ((e = hipEventCreate(&t0)) != hipSuccess) return e;
-  if ((e = hipEventCreate(&t1)) != hipSuccess) {
-    (void)hipEventDestroy(t0);
-    return e;
-  }
-  hipLaunchKernelGGL(mfma_rate_kernel, dim3(blocks), dim3(256), 0, stream, iters);   // warm-up
-  (void)hipEventRecord(t0, stream);
-  hipLaunchKernelGGL(mfma_rate_kernel, dim3(blocks), dim3(256), 0, stream, iters);
-  (void)hipEventRecord(t1, stream);
-  e = hipGetLastError();
-  if (e == hipSuccess) e = hipEventSynchronize(t1);
-  float ms = 0.f;
-  if (e == hipSuccess) e = hipEventElapsedTime(&ms, t0, t1);
-  (void)hipEventDestroy(t0);
-  (void)hipEventDestroy(t1);
-  if (e != hipSuccess) return e;
-  const double flops = (double)blocks * 4 * iters * 8 * (32.0 * 32 * 16 * 2);
-  *tflops = ms > 0.f ? flops / (ms * 1e-3) / 1e12 : 0.0;
-  return hipSuccess;
-}
-
 // Explicit instantiations: every kernel the launchers use is emitted, with its host stub.
 template __global__ void fwd_kernel<64>(RowArgs);
 template __global__ void fwd_kernel<128>(RowArgs);

@@ -77,9 +77,6 @@ hipError_t launch_paged_append(const void* kn, const void* vn, const int* pos, c
 hipError_t launch_paged_evict(const int* slots, int n, int* slot_pos, int num_slots, hipStream_t stream);
 hipError_t launch_paged_decode(const PagedDecode& p);
 
-// Measured dense bf16 MFMA rate of the current device (TFLOP/s); synchronous.
-hipError_t measure_mfma_rate(double* tflops, hipStream_t stream);
-
 // Per-kernel event bracketing (benchmark timing).
 void prof_begin(const char* name, hipStream_t s);
 void prof_end(hipStream_t s);

@@ -50,7 +50,6 @@ SIGNATURES = {
     "kvs_prof_enable": (None, [_I]),
     "kvs_prof_reset": (None, []),
     "kvs_prof_read": (_I, [ctypes.c_char_p, ctypes.POINTER(_I), ctypes.POINTER(ctypes.c_double)]),
-    "kvs_measure_mfma_rate": (_I, [ctypes.POINTER(ctypes.c_double), _P]),
     # streamed paged KV cache (host block manager: host int32 arrays)
     "kvs_bm_create": (_I, [_I, _I, _I, _I, ctypes.POINTER(_P)]),
     "kvs_bm_destroy": (None, [_P]),
@@ -268,14 +267,6 @@ def kvs_check_evict_at(evict_at, cu_seqlens=None) -> int:
         return int(fb.value)
     _check("kvs_check_evict_at", st)
     return -1
-
-
-def kvs_measure_mfma_rate() -> float:
-    """Measured dense bf16 MFMA rate of the current device in TFLOP/s (synchronous)."""
-    out = ctypes.c_double(0.0)
-    stream = torch.cuda.current_stream().cuda_stream
-    _check("kvs_measure_mfma_rate", lib.kvs_measure_mfma_rate(ctypes.byref(out), stream))
-    return float(out.value)
 
 
 def kvs_prof_enable(on: bool) -> None:

@@ -136,5 +136,10 @@ def test_prof_read_without_records(kvs):
     assert kvs.kvs_prof_read("fwd") == (0, 0.0)
 
 
-def test_mfma_rate_probe_validation(kvs):
-    assert kvs.lib.kvs_measure_mfma_rate(None, None) == 1   # KVS_ERR_NULL before any HIP call
+def test_bench_probe_is_outside_the_library(kvs):
+    """The matrix-core probe lives in the benchmark's own library, not in the libkvs ABI."""
+    assert not hasattr(ctypes.CDLL(LIB), "kvs_measure_mfma_rate")
+    probe = os.path.join(ROOT, "paper_2609_35750_amd", "libkvs_bench.so")
+    lib = ctypes.CDLL(probe)
+    lib.kvs_bench_mfma_rate.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    assert lib.kvs_bench_mfma_rate(None, None) == 1   # NULL result pointer, before any HIP call
