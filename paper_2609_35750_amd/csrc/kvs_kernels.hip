@@ -154,24 +154,28 @@ __global__ void __launch_bounds__(256) check_kernel(const int* __restrict__ evic
 // ---------------------------------------------------------------- key-tile walker
 // Every wave of a workgroup walks the same sequence of non-EMPTY key tiles of
 // its query rows [i0, i1): 64 candidate tiles are classified at a time (one
-// per lane) and the results kept as two ballots.
+// per lane) and the non-EMPTY ones kept as a ballot.  Each lane keeps the
+// evict_at statistics of its candidate tile, so the statistics of the tile
+// walker_next returns are read from a register (walker_stats) instead of from
+// memory, whose latency the wave would otherwise wait out on every tile.
 struct TileWalker {
   int base, lim;
-  unsigned long long live, full;
+  unsigned long long live;
+  int emin, emax;   // statistics of candidate tile base + lane
 };
 
 __device__ __forceinline__ void walker_load(TileWalker& w, const int2* __restrict__ ks, int kidx0, int i0, int i1,
                                             int L, int flags) {
   const int kt = w.base + (threadIdx.x & 63);
-  bool ne = false, fu = false;
+  bool ne = false;
+  int2 st = make_int2(0, 0);
   if (kt < w.lim) {
-    const int2 st = ks[kidx0 + kt];
-    const int c = adjust_class(tile_class(i0, i1, kt * kKeyTile, kt * kKeyTile + kKeyTile, L, st.x, st.y), flags);
-    ne = c != kEmpty;
-    fu = c == kFull;
+    st = ks[kidx0 + kt];
+    ne = adjust_class(tile_class(i0, i1, kt * kKeyTile, kt * kKeyTile + kKeyTile, L, st.x, st.y), flags) != kEmpty;
   }
   w.live = __ballot(ne);
-  w.full = __ballot(fu);
+  w.emin = st.x;
+  w.emax = st.y;
 }
 
 __device__ __forceinline__ int walker_next(TileWalker& w, const int2* __restrict__ ks, int kidx0, int i0, int i1,
@@ -184,6 +188,12 @@ __device__ __forceinline__ int walker_next(TileWalker& w, const int2* __restrict
   const int bit = __builtin_ctzll(w.live);
   w.live &= w.live - 1ull;
   return w.base + bit;
+}
+
+// evict_at minimum and maximum of tile kt, the tile the last walker_next call returned (kt >= 0)
+__device__ __forceinline__ int2 walker_stats(const TileWalker& w, int kt) {
+  const int l = kt - w.base;
+  return make_int2(__builtin_amdgcn_readlane(w.emin, l), __builtin_amdgcn_readlane(w.emax, l));
 }
 
 // ---------------------------------------------------------------- operand reads from swizzled tiles
@@ -330,16 +340,16 @@ fwd_kernel(RowArgs a) {
   const float inv_scale_log2 = 1.f / a.scale_log2;
 
   const int kidx0 = kstat_index(rt.b, tr.tok0, 0, kKeyTile);
-  TileWalker w{0, (min(rt.i1, tr.L) + kKeyTile - 1) / kKeyTile, 0ull, 0ull};
+  TileWalker w{0, (min(rt.i1, tr.L) + kKeyTile - 1) / kKeyTile, 0ull, 0, 0};
   walker_load(w, a.kstats, kidx0, rt.i0, rt.i1, tr.L, a.flags);
   int kt = __builtin_amdgcn_readfirstlane(walker_next(w, a.kstats, kidx0, rt.i0, rt.i1, tr.L, a.flags));
-  int2 kst = kt >= 0 ? a.kstats[kidx0 + kt] : make_int2(0, 0);
+  int2 kst = kt >= 0 ? walker_stats(w, kt) : make_int2(0, 0);
   int sub = 0;
 
   // One tile: prefetch the next tile into (nK, nV, nE), compute on (cK, cV, cE).
   auto body = [&](const uint16_t* cK, const uint16_t* cV, const int* cE, uint16_t* nK, uint16_t* nV, int* nE) {
-    // Statistics of the next tile are read before its copy is issued and used one
-    // iteration later, so no wait on this iteration's copies is needed for them.
+    // The next tile's statistics come from the walker's registers (no memory
+    // access) and are used one iteration later.
     int nkt = kt, nsub = sub + 1;
     int2 nkst = kst;
     // next 64-key tile once this one is done or its remaining keys lie past the trace end
@@ -347,7 +357,7 @@ fwd_kernel(RowArgs a) {
     if (nsub == NSUB || kt * kKeyTile + nsub * BN >= tr.L) {
       nkt = __builtin_amdgcn_readfirstlane(walker_next(w, a.kstats, kidx0, rt.i0, rt.i1, tr.L, a.flags));
       nsub = 0;
-      if (nkt >= 0) nkst = a.kstats[kidx0 + nkt];
+      if (nkt >= 0) nkst = walker_stats(w, nkt);
     }
     if (nkt >= 0) stage(nK, nV, nE, nkt, nsub);
     const int j0 = kt * kKeyTile + sub * BN;
@@ -515,18 +525,18 @@ __global__ void __launch_bounds__(512) dq_kernel(RowArgs a) {
   for (int d = 0; d < DB; ++d) acc[d] = f32x16{};
 
   const int kidx0 = kstat_index(rt.b, tr.tok0, 0, kKeyTile);
-  TileWalker w{0, (min(rt.i1, tr.L) + kKeyTile - 1) / kKeyTile, 0ull, 0ull};
+  TileWalker w{0, (min(rt.i1, tr.L) + kKeyTile - 1) / kKeyTile, 0ull, 0, 0};
   walker_load(w, a.kstats, kidx0, rt.i0, rt.i1, tr.L, a.flags);
   int kt = __builtin_amdgcn_readfirstlane(walker_next(w, a.kstats, kidx0, rt.i0, rt.i1, tr.L, a.flags));
-  int2 kst = kt >= 0 ? a.kstats[kidx0 + kt] : make_int2(0, 0);
+  int2 kst = kt >= 0 ? walker_stats(w, kt) : make_int2(0, 0);
 
   auto body = [&](const uint16_t* cK, const uint16_t* cV, const int* cE, uint16_t* nK, uint16_t* nV, int* nE) {
-    // Statistics of the next tile are read before its copy is issued and used one
-    // iteration later, so no wait on this iteration's copies is needed for them.
+    // The next tile's statistics come from the walker's registers (no memory
+    // access) and are used one iteration later.
     const int nkt = __builtin_amdgcn_readfirstlane(walker_next(w, a.kstats, kidx0, rt.i0, rt.i1, tr.L, a.flags));
     int2 nkst = make_int2(0, 0);
     if (nkt >= 0) {
-      nkst = a.kstats[kidx0 + nkt];
+      nkst = walker_stats(w, nkt);
       stage_kv<D>(kvst, nK, nV, nE, a, rt, nkt, wave, nw, lane);
     }
     const int j0 = kt * kKeyTile;
