@@ -257,19 +257,23 @@ __device__ __forceinline__ bf16x8 tr_operand(const uint16_t* tile, int row0, int
 // Asynchronous global -> LDS copies of an R-row tile (dma_b128:
 // lane l of a wave writes 16 bytes at the wave's LDS base + 16 l, so the 64
 // lanes of one instruction fill 64 consecutive 16-byte slots of the padded
-// tile; padding slots are skipped).  Waves take turns issuing the 64-slot
-// pieces: wave w issues pieces w, w + nw, ...  The per-lane tile row and column
-// of every piece are computed once (init) so that issuing a tile costs a
-// clamp and an address per piece.  Row r of the tile comes from global row
-// min(row0 + r, rmax) (rows past the end of a trace repeat its last row;
-// callers mask them).  Lanes whose slot is row padding copy the row's first
-// chunk into it (padding is never read), so no lane is switched off.
-template <int D, int R, int MAXI, bool COMPACT = false>
+// tile).  The NW waves of a workgroup take turns issuing the 64-slot pieces:
+// wave w issues pieces w, w + NW, ...  The per-lane source offset of every
+// piece is computed once (init).  Issuing a tile is one unsigned min and one
+// copy per piece, with no branch but the wave's last piece when NW does not
+// divide the piece count (a taken branch costs a wave tens of clocks; the
+// copies of one tile used to sit behind a dozen of them).  Rows past the end
+// of a trace (row0 + r > rmax) all read the last 16 bytes of row rmax, a valid
+// address; their values are never used unmasked (callers mask rows and keys
+// past the trace end, and multiply them by exact zeros).  Lanes whose slot is
+// row padding copy the row's first chunk into it (padding is never read).
+template <int D, int R, int NW, bool COMPACT = false>
 struct RowStager {
   using LY = Lay<D, COMPACT>;
   static constexpr int NI = R * LY::CPRP / kWave;   // 64-slot pieces per tile
+  static constexpr int PW = (NI + NW - 1) / NW;      // pieces per wave (the last one conditional)
   static_assert(R * LY::CPRP % kWave == 0, "tile must fill whole 64-slot pieces");
-  uint32_t off[MAXI];   // byte offset of the slot's source from the tile's first row (no clamping)
+  uint32_t off[PW];   // byte offset of the slot's source from the tile's first row (no clamping)
 
   // tile row and source element column of this lane's slot in piece n
   __device__ static __forceinline__ void slot(int n, int lane, int& r, int& col) {
@@ -278,38 +282,27 @@ struct RowStager {
     const int pc = q - r * LY::CPRP;
     col = pc < LY::CPR ? 8 * (pc ^ LY::flip(r)) : 0;
   }
-  __device__ __forceinline__ void init(int wave, int nw, int lane, long long row_stride) {
+  __device__ __forceinline__ void init(int wave, int lane, long long row_stride) {
 #pragma unroll
-    for (int i = 0; i < MAXI; ++i) {
-      const int n = wave + i * nw;
+    for (int i = 0; i < PW; ++i) {
+      const int n = wave + i * NW;
       int r, col;
       slot(n, lane, r, col);
       off[i] = n < NI ? (uint32_t)(r * row_stride + col) * 2u : 0u;
     }
   }
-  // row0 <= rmax; rows row0 .. row0 + R - 1 of g (clamped) span less than 4 GiB; row_stride as given to init().
+  // row0 <= rmax; rows row0 .. min(row0 + R - 1, rmax) of g span less than 4 GiB; row_stride as given to init().
   // lds: LDS byte address of the tile (lds_addr).
   __device__ __forceinline__ void issue(uint32_t lds, const uint16_t* __restrict__ g, long long row_stride, int row0,
-                                        int rmax, int wave, int nw) const {
+                                        int rmax, int wave) const {
     const uint16_t* base = uniform_ptr(g + (long long)row0 * row_stride);
-    if (row0 + R - 1 <= rmax) {   // whole tile inside: precomputed offsets
+    const int dr = rmax - row0;
+    // a slot of a row past rmax has an offset above lim (row_stride >= D); valid rows stay at or below it
+    const uint32_t lim = dr >= R - 1 ? 0xffffffffu : (uint32_t)(dr * row_stride + D - 8) * 2u;
 #pragma unroll
-      for (int i = 0; i < MAXI; ++i) {
-        const int n = wave + i * nw;
-        if (n < NI) dma_b128(base, off[i], lds + n * kWave * 16);
-      }
-    } else {
-      const int lane = threadIdx.x & (kWave - 1);
-#pragma unroll
-      for (int i = 0; i < MAXI; ++i) {
-        const int n = wave + i * nw;
-        if (n < NI) {
-          int r, col;
-          slot(n, lane, r, col);
-          const int dr = min(row0 + r, rmax) - row0;
-          dma_b128(base, (uint32_t)(dr * row_stride + col) * 2u, lds + n * kWave * 16);
-        }
-      }
+    for (int i = 0; i < PW; ++i) {
+      const int n = wave + i * NW;
+      if (i < PW - 1 || NI % NW == 0 || n < NI) dma_b128(base, min(off[i], lim), lds + n * kWave * 16);
     }
   }
 };

@@ -260,7 +260,7 @@ __device__ __forceinline__ bool row_tile(const RowArgs& a, RowTile& t) {
 // Asynchronous staging of one 64-key K/V (and evict_at) tile of KV head g
 // (compact layout: two workgroups of the dQ kernel share a CU).
 template <int D>
-using KVStager = RowStager<D, kKeyTile, (kKeyTile * Lay<D, true>::CPRP / kWave + 3) / 4, true>;   // >= 4 waves
+using KVStager = RowStager<D, kKeyTile, 4, true>;   // row kernels: 4 waves
 
 template <int D>
 __device__ __forceinline__ void stage_kv(const KVStager<D>& st, uint16_t* sK, uint16_t* sV, int* sE, const RowArgs& a,
@@ -268,8 +268,8 @@ __device__ __forceinline__ void stage_kv(const KVStager<D>& st, uint16_t* sK, ui
   const int j0 = kt * kKeyTile;
   const long long base = ((long long)rt.tr.tok0 * a.Hkv + rt.g) * D;
   const long long stride = (long long)a.Hkv * D;
-  st.issue(lds_addr(sK), a.k + base, stride, j0, rt.tr.L - 1, wave, nw);
-  st.issue(lds_addr(sV), a.v + base, stride, j0, rt.tr.L - 1, wave, nw);
+  st.issue(lds_addr(sK), a.k + base, stride, j0, rt.tr.L - 1, wave);
+  st.issue(lds_addr(sV), a.v + base, stride, j0, rt.tr.L - 1, wave);
   if (wave == nw - 1) stage_words(lds_addr(sE), a.evict + rt.tr.tok0, j0, rt.tr.L - 1, lane);
 }
 
@@ -287,7 +287,7 @@ template <int D>
 constexpr int fwd_bn() { return D == 128 ? 32 : 64; }
 
 template <int D>
-using FwdStager = RowStager<D, fwd_bn<D>(), (fwd_bn<D>() * Lay<D, true>::CPRP / kWave + 3) / 4, true>;   // >= 4 waves
+using FwdStager = RowStager<D, fwd_bn<D>(), 4, true>;   // 4 waves
 
 template <int D>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 128 ? 3 : 2, D == 128 ? 3 : 2)))
@@ -310,14 +310,14 @@ fwd_kernel(RowArgs a) {
   const auto rl = Lay<D, true>::row_lane(lane);
   const int tl = Lay<D, true>::tr_lo(lane), th = Lay<D, true>::tr_hi(lane);
   FwdStager<D> kvst;
-  kvst.init(wave, nw, lane, (long long)a.Hkv * D);
+  kvst.init(wave, lane, (long long)a.Hkv * D);
   // asynchronous staging of sub-tile (kt, sub) of KV head g
   auto stage = [&](uint16_t* sK, uint16_t* sV, int* sE, int kt, int sub) __attribute__((always_inline)) {
     const int j0 = kt * kKeyTile + sub * BN;
     const long long base = ((long long)rt.tr.tok0 * a.Hkv + rt.g) * D;
     const long long stride = (long long)a.Hkv * D;
-    kvst.issue(lds_addr(sK), a.k + base, stride, j0, rt.tr.L - 1, wave, nw);
-    kvst.issue(lds_addr(sV), a.v + base, stride, j0, rt.tr.L - 1, wave, nw);
+    kvst.issue(lds_addr(sK), a.k + base, stride, j0, rt.tr.L - 1, wave);
+    kvst.issue(lds_addr(sV), a.v + base, stride, j0, rt.tr.L - 1, wave);
     if (wave == nw - 1) {
       if (BN == kWave || lane < BN) stage_words(lds_addr(sE), a.evict + rt.tr.tok0, j0, rt.tr.L - 1, lane);
     }
@@ -503,7 +503,7 @@ __global__ void __launch_bounds__(512) dq_kernel(RowArgs a) {
   const auto rl = Lay<D, true>::row_lane(lane);
   const int tl = Lay<D, true>::tr_lo(lane), th = Lay<D, true>::tr_hi(lane);
   KVStager<D> kvst;
-  kvst.init(wave, nw, lane, (long long)a.Hkv * D);
+  kvst.init(wave, lane, (long long)a.Hkv * D);
   const int ic = min(i, tr.L - 1);
 
   bf16x8 qreg[KS], oreg[KS];
@@ -656,8 +656,8 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
     emax_w = max(emax_w, __shfl_xor(emax_w, off));
   }
   if (!role_dk && lane == 0) sEmax[kw] = emax_w;
-  RowStager<D, kQStep, 3> qst;
-  qst.init(wave, 8, lane, (long long)a.Hq * D);
+  RowStager<D, kQStep, 8> qst;
+  qst.init(wave, lane, (long long)a.Hq * D);
 
   // K (dV waves) or V (dK waves) of this lane's key: the B operand of S or dP
   bf16x8 kvreg[KS];
@@ -685,8 +685,8 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
     const int i0 = (qs_lo + step / a.G) * kQStep;
     const int h = g * a.G + step % a.G;
     const long long base = ((long long)tr.tok0 * a.Hq + h) * D;
-    qst.issue(lds_addr(q_), a.q + base, (long long)a.Hq * D, i0, tr.L - 1, wave, 8);
-    qst.issue(lds_addr(o_), a.dout + base, (long long)a.Hq * D, i0, tr.L - 1, wave, 8);
+    qst.issue(lds_addr(q_), a.q + base, (long long)a.Hq * D, i0, tr.L - 1, wave);
+    qst.issue(lds_addr(o_), a.dout + base, (long long)a.Hq * D, i0, tr.L - 1, wave);
     const long long lb = lse_index(a.varlen, a.ntok, a.Hq, a.T, b, h, tr.tok0, 0);
     if (wave == 6) stage_words(lds_addr(l_), a.lse + lb, i0, tr.L - 1, lane);   // LSE * log2(e)
     if (wave == 7) stage_words(lds_addr(d_), a.delta + lb, i0, tr.L - 1, lane);
