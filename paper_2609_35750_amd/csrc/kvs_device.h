@@ -261,8 +261,8 @@ __device__ __forceinline__ bf16x8 tr_operand(const uint16_t* tile, int row0, int
 // wave w issues pieces w, w + NW, ...  The per-lane source offset of every
 // piece is computed once (init).  Issuing a tile is one unsigned min and one
 // copy per piece, with no branch but the wave's last piece when NW does not
-// divide the piece count (a taken branch costs a wave tens of clocks; the
-// copies of one tile used to sit behind a dozen of them).  Rows past the end
+// divide the piece count (a taken branch costs a wave tens of clocks, and the
+// copies sit at the start of every tile step).  Rows past the end
 // of a trace (row0 + r > rmax) all read the last 16 bytes of row rmax, a valid
 // address; their values are never used unmasked (callers mask rows and keys
 // past the trace end, and multiply them by exact zeros).  Lanes whose slot is
