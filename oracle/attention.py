@@ -234,3 +234,52 @@ def dq_rounding_scale(q, k, v, evict_at, scale, do, rows, cu_seqlens=None):
                 out[idx, h, :] = scale * (np.abs(dS) @ np.abs(k[a:a + j1, g, :])
                                           + np.abs(P @ k[a:a + j1, g, :]) * R)
     return out
+
+
+def dkdv_rounding_rss(q, k, v, evict_at, scale, do, cu_seqlens=None):
+    """Root-sum-square sensitivity of dK and dV to the roundings every bf16 backward makes.
+
+    ``dV_jd = sum_{h in g} sum_i P_hij dO_hid`` takes P rounded to bf16, and
+    ``dK_jd = scale sum_{h in g} sum_i dS_hij q_hid`` takes dS rounded to bf16,
+    with ``dS_hij = P_hij (dP_hij - Delta_hi)`` and ``Delta_hi`` formed from the
+    bf16 O.  Each rounding is a relative error of at most u, and the sums run
+    over many rows and heads whose roundings are independent, so the error of
+    a sum is of the order of u times the root sum of squares of its terms
+    (probabilistic rounding-error analysis, Higham and Mary, SIAM J. Sci.
+    Comput. 41(5), 2019), not u times the sum of their magnitudes:
+
+        SV_jd = sqrt( sum_{h in g} sum_i (P_hij dO_hid)^2 )
+        SK_jd = scale * sqrt( sum_{h in g} sum_i ( dS_hij^2 + (P_hij R_hi)^2 ) q_hid^2 ),
+        R_hi  = sqrt( sum_d' (dO_hid' O_hid')^2 )   (the rounding of O reaching Delta)
+
+    (g: the KV head of key j; i over the rows that see key j).  Returns
+    ``(SK, SV)`` (fp64), each shaped like k.  Test infrastructure for
+    tolerances: P, dS and O are the exact quantities of the definitions above.
+    """
+    q, k, v, do = _f64(q), _f64(k), _f64(v), _f64(do)
+    e = np.asarray(evict_at, dtype=np.int64)
+    n, Hq, D = q.shape
+    G = Hq // k.shape[1]
+    SK2 = np.zeros_like(k)
+    SV2 = np.zeros_like(v)
+    for a, b in _split(cu_seqlens, n):
+        L = b - a
+        if L == 0:
+            continue
+        for i0 in range(0, L, ROW_BLOCK):
+            i1 = min(i0 + ROW_BLOCK, L)
+            M = visible_mask(e[a:b], L, i0, i1, i1)
+            for h in range(Hq):
+                g = h // G
+                S = np.where(M, scale * (q[a + i0:a + i1, h, :] @ k[a:a + i1, g, :].T), -np.inf)
+                m = S.max(axis=1, keepdims=True)
+                E = np.where(M, np.exp(S - m), 0.0)
+                P = E / E.sum(axis=1, keepdims=True)
+                dP = do[a + i0:a + i1, h, :] @ v[a:a + i1, g, :].T
+                dlt = (P * dP).sum(axis=1, keepdims=True)
+                dS = P * (dP - dlt)
+                O = P @ v[a:a + i1, g, :]
+                R2 = ((do[a + i0:a + i1, h, :] * O) ** 2).sum(axis=1, keepdims=True)
+                SV2[a:a + i1, g, :] += (P ** 2).T @ (do[a + i0:a + i1, h, :] ** 2)
+                SK2[a:a + i1, g, :] += (dS ** 2 + P ** 2 * R2).T @ (q[a + i0:a + i1, h, :] ** 2)
+    return scale * np.sqrt(SK2), np.sqrt(SV2)

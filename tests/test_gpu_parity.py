@@ -36,9 +36,11 @@ def _parity(kvs, wl, e, cu=None, B=None, switches=True):
     cu_ref = cu if cu is not None else (np.arange(B + 1) * wl.lengths[0] if B else None)
     ref = orc.backward(t["q"], t["k"], t["v"], e, scale, t["do"], cu_seqlens=cu_ref)
     E = orc.dq_rounding_scale(t["q"], t["k"], t["v"], e, scale, t["do"], np.arange(wl.ntok), cu_seqlens=cu_ref)
+    SK, SV = orc.dkdv_rounding_rss(t["q"], t["k"], t["v"], e, scale, t["do"], cu_seqlens=cu_ref)
     out = {}
     for key in ("O", "dq", "dk", "dv"):
-        out[key] = assert_close(f"{wl.name}:{key}", to_f64(res[key]), ref[key], E=E if key == "dq" else None)
+        out[key] = assert_close(f"{wl.name}:{key}", to_f64(res[key]), ref[key], E=E if key == "dq" else None,
+                                S={"dk": SK, "dv": SV}.get(key))
     assert_lse(wl.name, to_f64(res["LSE"]), ref["LSE"])
     if switches:
         assert_switches_bitwise(kvs, res, t["q"], t["k"], t["v"], t["do"], e, scale, cu_seqlens=cu, max_seqlen=mx,
@@ -74,6 +76,27 @@ LAYOUT_CASES = [
 def test_layouts(kvs, case):
     L, Hq, Hkv, D, p, w, s, strat = case
     wl = inputs.custom_workload(f"layout_L{L}", Hq, Hkv, D, [L], p, w, s, strat, seed=L)
+    _parity(kvs, wl, wl.evict_at())
+
+
+# Head-group shapes away from the benchmarked ones: the row kernels' head grouping
+# (4, 2 or 1 q-heads per workgroup, whichever divides G), the dK/dV kernel's
+# G q-heads per KV head, KV-head counts that are not a multiple of the 8 XCDs,
+# and the largest group size the library accepts (64).
+GROUP_CASES = [
+    # (L, Hq, Hkv, D)
+    (300, 32, 2, 128),   # G = 16
+    (257, 12, 12, 64),   # G = 1, 12 KV heads
+    (200, 64, 1, 64),    # G = 64
+    (333, 24, 8, 128),   # G = 3
+    (190, 14, 2, 128),   # G = 7
+]
+
+
+@pytest.mark.parametrize("case", GROUP_CASES, ids=lambda c: f"L{c[0]}_H{c[1]}x{c[2]}_D{c[3]}")
+def test_group_shapes(kvs, case):
+    L, Hq, Hkv, D = case
+    wl = inputs.custom_workload(f"group_L{L}_G{Hq // Hkv}", Hq, Hkv, D, [L], 9, 41, 7, "last2", seed=L + Hq)
     _parity(kvs, wl, wl.evict_at())
 
 

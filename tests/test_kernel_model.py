@@ -25,6 +25,13 @@ parity bound derived from it.
   The dQ bound therefore adds the first-order effect of those two roundings,
   2^-8 E with E = oracle.attention.dq_rounding_scale (2^-8: the relative
   rounding error bound of bf16).
+* dK and dV sum over the G q-heads of their group as well as over rows.  With
+  G = 16 or 64 the rounded P, dS and O (through Delta) leave the model's dK
+  and dV up to 1.5 times the bound above; the errors of the many independent
+  roundings add like a random walk, so the dK/dV bound adds
+  lambda 2^-8 S with S = oracle.attention.dkdv_rounding_rss (the root sum of
+  squares of the rounded terms) and lambda = 7 (Hoeffding: at most 5e-11 per
+  element); the model needs under a tenth of that.
 """
 import numpy as np
 import pytest
@@ -32,7 +39,7 @@ import pytest
 from oracle import attention as orc
 from paper_2609_35750_amd import inputs
 from tests import kernel_model as km
-from tests.gpu_helpers import DQ_GAMMA, MAX_ABS, REL_L2, ULP_FACTOR
+from tests.gpu_helpers import DQ_GAMMA, MAX_ABS, REL_L2, RSS_LAMBDA, U_BF16, ULP_FACTOR
 
 KEYS = (("O", "O"), ("dQ", "dq"), ("dK", "dk"), ("dV", "dv"))
 
@@ -133,3 +140,27 @@ def test_unguarded_rescale_gives_nan_rows_and_guard_fixes_them():
             assert np.isfinite(good[key]).all(), (D, key)
         ref = orc.forward(t["q"], t["k"], t["v"], e, wl.softmax_scale)
         assert np.abs(good["O"] - ref[0]).max() < MAX_ABS
+
+
+# Large GQA groups (dK/dV sum 16 and 64 q-heads), scaled down.
+GROUP_CASES = {
+    "group16": inputs.custom_workload("g16", 32, 2, 128, [300], 9, 41, 7, "last2", seed=332),
+    "group64": inputs.custom_workload("g64", 64, 1, 64, [200], 9, 41, 7, "last2", seed=264),
+}
+
+
+def test_dkdv_rounding_term_needed_for_large_groups_and_sufficient():
+    for name, wl in GROUP_CASES.items():
+        model, t, e, cu = _run(wl)
+        ref = orc.backward(t["q"], t["k"], t["v"], e, wl.softmax_scale, t["do"], cu_seqlens=cu)
+        SK, SV = orc.dkdv_rounding_rss(t["q"], t["k"], t["v"], e, wl.softmax_scale, t["do"], cu_seqlens=cu)
+        worst_plain, worst_lam = 0.0, 0.0
+        for key, S in (("dk", SK), ("dv", SV)):
+            d = np.abs(model[key] - ref[key])
+            plain = MAX_ABS + ULP_FACTOR * km.ulp_bf16(ref[key])
+            worst_plain = max(worst_plain, float((d / plain).max()))
+            lam = float((np.maximum(d - plain, 0.0) / (U_BF16 * S)).max())
+            worst_lam = max(worst_lam, lam)
+            print(f"{name}:{key} worst / plain bound {float((d / plain).max()):.3f}, lambda needed {lam:.3f}")
+        assert worst_plain > 1.0, (name, worst_plain)          # the plain bound does not hold
+        assert 0.0 < worst_lam <= RSS_LAMBDA / 10, (name, worst_lam)

@@ -368,3 +368,57 @@ def test_dq_rounding_scale_closed_forms():
     Ev = orc.dq_rounding_scale(q, k, v, np.r_[np.full(4, 4), np.full(5, 5)], scale, do, np.arange(L), cu)
     np.testing.assert_allclose(Ev[:4], orc.dq_rounding_scale(q[:4], k[:4], v[:4], np.full(4, 4), scale, do[:4],
                                                              np.arange(4)), rtol=1e-12)
+
+
+def test_dkdv_rounding_rss_closed_forms():
+    """dkdv_rounding_rss against cases with a closed form.
+
+    * Every key visible only to itself (e_j = j + 1): P = I, dS = 0 and O_j = v_j,
+      so SV_jd = sqrt(sum_h dO_jhd^2) and SK_jd = scale sqrt(sum_h R_jh^2 q_jhd^2)
+      with R_jh^2 = sum_d' (dO_jhd' v_jd')^2 (sums over the q-heads h of the group).
+    * A causal trace of two tokens: key 1 is seen by row 1 alone, with the
+      two-key softmax weight p1 = 1 / (1 + exp(s_10 - s_11)) and
+      dS_11 = p0 p1 (dP_11 - dP_10), so SV_1d = sqrt(sum_h (p1 dO_1hd)^2) and
+      SK_1d = scale sqrt(sum_h (dS_11^2 + p1^2 R_1h^2) q_1hd^2) with O_1 = p0 v_0 + p1 v_1.
+    * The squares add over the q-heads of a group: one KV head with G q-heads
+      gives the root of the sum of the G single-head squares; varlen traces are
+      independent.
+    """
+    rng = np.random.default_rng(6)
+    L, Hq, Hkv, D, scale = 9, 4, 2, 8, 0.41
+    q, k, v, do = (rng.standard_normal(s) for s in [(L, Hq, D), (L, Hkv, D), (L, Hkv, D), (L, Hq, D)])
+    G = Hq // Hkv
+    SK, SV = orc.dkdv_rounding_rss(q, k, v, np.arange(1, L + 1), scale, do)
+    for g in range(Hkv):
+        hs = range(g * G, (g + 1) * G)
+        sv = np.sqrt(sum(do[:, h] ** 2 for h in hs))
+        R2 = [((do[:, h] * v[:, g]) ** 2).sum(axis=1, keepdims=True) for h in hs]
+        sk = scale * np.sqrt(sum(r2 * q[:, h] ** 2 for r2, h in zip(R2, hs)))
+        np.testing.assert_allclose(SV[:, g], sv, rtol=1e-12)
+        np.testing.assert_allclose(SK[:, g], sk, rtol=1e-12)
+    SK, SV = orc.dkdv_rounding_rss(q[:2], k[:2], v[:2], np.full(2, 2), scale, do[:2])
+    for g in range(Hkv):
+        sv2, sk2 = 0.0, 0.0
+        for h in range(g * G, (g + 1) * G):
+            s0, s1 = scale * q[1, h] @ k[0, g], scale * q[1, h] @ k[1, g]
+            p1 = 1.0 / (1.0 + math.exp(s0 - s1))
+            p0 = 1.0 - p1
+            ds = p0 * p1 * (do[1, h] @ v[1, g] - do[1, h] @ v[0, g])
+            O1 = p0 * v[0, g] + p1 * v[1, g]
+            R2 = ((do[1, h] * O1) ** 2).sum()
+            sv2 = sv2 + (p1 * do[1, h]) ** 2
+            sk2 = sk2 + (ds ** 2 + p1 ** 2 * R2) * q[1, h] ** 2
+        np.testing.assert_allclose(SV[1, g], np.sqrt(sv2), rtol=1e-10)
+        np.testing.assert_allclose(SK[1, g], scale * np.sqrt(sk2), rtol=1e-10)
+    causal = np.full(L, L)
+    SK, SV = orc.dkdv_rounding_rss(q, k, v, causal, scale, do)
+    for g in range(Hkv):
+        parts = [orc.dkdv_rounding_rss(q[:, h:h + 1], k[:, g:g + 1], v[:, g:g + 1], causal, scale, do[:, h:h + 1])
+                 for h in range(g * G, (g + 1) * G)]
+        np.testing.assert_allclose(SK[:, g], np.sqrt(sum(p[0][:, 0] ** 2 for p in parts)), rtol=1e-12)
+        np.testing.assert_allclose(SV[:, g], np.sqrt(sum(p[1][:, 0] ** 2 for p in parts)), rtol=1e-12)
+    cu = np.array([0, 4, 9])
+    SKv, SVv = orc.dkdv_rounding_rss(q, k, v, np.r_[np.full(4, 4), np.full(5, 5)], scale, do, cu)
+    SK4, SV4 = orc.dkdv_rounding_rss(q[:4], k[:4], v[:4], np.full(4, 4), scale, do[:4])
+    np.testing.assert_allclose(SKv[:4], SK4, rtol=1e-12)
+    np.testing.assert_allclose(SVv[:4], SV4, rtol=1e-12)
