@@ -25,10 +25,13 @@ def kvs():
     return k
 
 
-def _parity(kvs, wl, e, cu=None, B=None, switches=True):
+def _parity(kvs, wl, e, cu=None, B=None, switches=True, q_mul=None):
     """Element by element against the checker; then the tile-classifier
-    switches must leave every output bit-identical."""
+    switches must leave every output bit-identical.  q_mul (a power of two, so
+    the bf16 query stays exact) widens the logits."""
     t = inputs.make_tensors(wl)
+    if q_mul is not None:
+        t["q"] = t["q"] * q_mul
     scale = wl.softmax_scale
     announce(f"{wl.name} lengths={wl.lengths} Hq={wl.Hq} Hkv={wl.Hkv} D={wl.D} varlen={cu is not None} B={B}")
     mx = max(wl.lengths) if cu is not None else None
@@ -98,6 +101,16 @@ def test_group_shapes(kvs, case):
     L, Hq, Hkv, D = case
     wl = inputs.custom_workload(f"group_L{L}_G{Hq // Hkv}", Hq, Hkv, D, [L], 9, 41, 7, "last2", seed=L + Hq)
     _parity(kvs, wl, wl.evict_at())
+
+
+@pytest.mark.parametrize("D", [128, 64])
+def test_large_logits(kvs, D):
+    """Scores 16 times wider than unit-variance inputs give (standard deviation
+    ~16 at scale 1/sqrt(D)): nearly one-hot softmax rows, exponentials far
+    below fp32 range, and a reference maximum that keeps moving by more than
+    the forward's lazy-rescale margin (8 in log2 units) as the walk proceeds."""
+    wl = inputs.custom_workload(f"wide_logits_D{D}", 8, 2, D, [700], 12, 60, 10, "last2", seed=700 + D)
+    _parity(kvs, wl, wl.evict_at(), q_mul=16.0)
 
 
 @pytest.mark.parametrize("L,Hq,Hkv,D,seed", [(130, 4, 2, 128, 1), (333, 2, 1, 64, 2), (515, 10, 2, 128, 3)])
