@@ -216,10 +216,10 @@ struct Lay {
   static constexpr int PITCH = D == 128 ? (COMPACT ? 144 : 160) : 72;   // bf16 elements per LDS row
   static constexpr int CPR = D / 8;                                   // 16-byte data chunks per row
   static constexpr int CPRP = PITCH / 8;                              // chunks per padded row
-  __device__ static __forceinline__ int flip(int r) {
+  __host__ __device__ static __forceinline__ int flip(int r) {
     return D == 128 ? (COMPACT ? ((r >> 3) & 1) : ((r >> 2) & 3)) : 0;
   }
-  __device__ static __forceinline__ int off(int r, int col) { return r * PITCH + (((col >> 3) ^ flip(r)) << 3) + (col & 7); }
+  __host__ __device__ static __forceinline__ int off(int r, int col) { return r * PITCH + (((col >> 3) ^ flip(r)) << 3) + (col & 7); }
   // b128 operand reads: row (row0 + l % 32), columns 16 ks + 8 (l / 32) .. +7.
   // (odd k-steps: chunk bit 1 toggled, i.e. the base XOR 16, since rows
   // start at multiples of 32 elements)
@@ -276,33 +276,40 @@ struct RowStager {
   uint32_t off[PW];   // byte offset of the slot's source from the tile's first row (no clamping)
 
   // tile row and source element column of this lane's slot in piece n
-  __device__ static __forceinline__ void slot(int n, int lane, int& r, int& col) {
+  __host__ __device__ static __forceinline__ void slot(int n, int lane, int& r, int& col) {
     const int q = n * kWave + lane;
     r = q / LY::CPRP;
     const int pc = q - r * LY::CPRP;
     col = pc < LY::CPR ? 8 * (pc ^ LY::flip(r)) : 0;
   }
+  // byte offset of the source of lane `lane`'s slot in piece n from the tile's first row (0 past the tile)
+  __host__ __device__ static __forceinline__ uint32_t src_offset(int n, int lane, long long row_stride) {
+    int r, col;
+    slot(n, lane, r, col);
+    return n < NI ? (uint32_t)(r * row_stride + col) * 2u : 0u;
+  }
+  // largest source offset of a tile whose last valid row is dr (= rmax - row0): the last 16 bytes of
+  // that row; a slot of a row past dr has a larger offset (row_stride >= D), valid rows a smaller one
+  __host__ __device__ static __forceinline__ uint32_t limit(int dr, long long row_stride) {
+    return dr >= R - 1 ? 0xffffffffu : (uint32_t)(dr * row_stride + D - 8) * 2u;
+  }
+  // whether piece i of a wave (piece number n) exists
+  __host__ __device__ static __forceinline__ bool issues(int i, int n) { return i < PW - 1 || NI % NW == 0 || n < NI; }
+
   __device__ __forceinline__ void init(int wave, int lane, long long row_stride) {
 #pragma unroll
-    for (int i = 0; i < PW; ++i) {
-      const int n = wave + i * NW;
-      int r, col;
-      slot(n, lane, r, col);
-      off[i] = n < NI ? (uint32_t)(r * row_stride + col) * 2u : 0u;
-    }
+    for (int i = 0; i < PW; ++i) off[i] = src_offset(wave + i * NW, lane, row_stride);
   }
   // row0 <= rmax; rows row0 .. min(row0 + R - 1, rmax) of g span less than 4 GiB; row_stride as given to init().
   // lds: LDS byte address of the tile (lds_addr).
   __device__ __forceinline__ void issue(uint32_t lds, const uint16_t* __restrict__ g, long long row_stride, int row0,
                                         int rmax, int wave) const {
     const uint16_t* base = uniform_ptr(g + (long long)row0 * row_stride);
-    const int dr = rmax - row0;
-    // a slot of a row past rmax has an offset above lim (row_stride >= D); valid rows stay at or below it
-    const uint32_t lim = dr >= R - 1 ? 0xffffffffu : (uint32_t)(dr * row_stride + D - 8) * 2u;
+    const uint32_t lim = limit(rmax - row0, row_stride);
 #pragma unroll
     for (int i = 0; i < PW; ++i) {
       const int n = wave + i * NW;
-      if (i < PW - 1 || NI % NW == 0 || n < NI) dma_b128(base, min(off[i], lim), lds + n * kWave * 16);
+      if (issues(i, n)) dma_b128(base, min(off[i], lim), lds + n * kWave * 16);
     }
   }
 };
