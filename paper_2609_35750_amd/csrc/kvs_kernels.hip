@@ -275,7 +275,8 @@ __device__ __forceinline__ void stage_kv(const KVStager<D>& st, uint16_t* sK, ui
 
 // ---------------------------------------------------------------- forward
 // K/V are staged in sub-tiles of BN keys (D = 128: 32, so that a workgroup
-// needs 37 KB of LDS and three workgroups share a CU; D = 64: 64), walked in
+// needs 37 KB of LDS and three workgroups, three waves per SIMD, share a CU;
+// D = 64: 64 keys, 37 KB, four workgroups at 128 VGPRs per wave), walked in
 // the order of the non-EMPTY 64-key tiles.  The sub-tiles are double-buffered
 // in two distinct LDS arrays each; the loop body alternates between them so
 // the compiler can tell that the asynchronous fill of the next buffer never
@@ -290,7 +291,7 @@ template <int D>
 using FwdStager = RowStager<D, fwd_bn<D>(), 4, true>;   // 4 waves
 
 template <int D>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 128 ? 3 : 2, D == 128 ? 3 : 2)))
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 128 ? 3 : 4, D == 128 ? 3 : 4)))
 fwd_kernel(RowArgs a) {
   constexpr int KS = D / 16, DB = D / 32, BN = fwd_bn<D>(), NKB = BN / 32, NSUB = kKeyTile / BN;
   __shared__ __attribute__((aligned(1024))) uint16_t sK0[BN * Lay<D, true>::PITCH];
