@@ -420,6 +420,8 @@ def main():
                     help="time replays of one step captured as a HIP graph (no host launch gaps)")
     ap.add_argument("--hq", type=int, default=0,
                     help="diagnostics: override the workload's q-head count (a multiple of its KV heads)")
+    ap.add_argument("--d", type=int, default=0, choices=(0, 64, 128),
+                    help="diagnostics: override the workload's head dimension (64 or 128)")
     ap.add_argument("--traffic-copy", action="store_true", help="run the 1 GiB copy that calibrates the counters")
     ap.add_argument("--traffic-summarize", nargs=2, metavar=("OUT", "WORKLOAD"),
                     help="summarise FETCH/WRITE counter runs under OUT into profiles/")
@@ -444,6 +446,8 @@ def main():
         if args.hq % wl.Hkv:
             sys.exit(f"--hq must be a multiple of the workload's {wl.Hkv} KV heads")
         wl = dataclasses.replace(wl, Hq=args.hq, name=f"{wl.name}_hq{args.hq}")
+    if args.d and args.d != wl.D:
+        wl = dataclasses.replace(wl, D=args.d, name=f"{wl.name}_d{args.d}")
     dev = torch.device("cuda:0")
     tensors = inputs.make_tensors(wl)
     e = wl.evict_at()
