@@ -44,6 +44,11 @@
  *  - `stream` is a hipStream_t (NULL = the null stream).  Calls only enqueue
  *    work on it and return; none synchronizes except kvs_check_evict_at.
  *  - Outputs are overwritten, never accumulated.
+ *  - An empty batch (Ntot = 0, e.g. varlen traces that are all empty) is
+ *    valid: shapes, softmax_scale and flags are still checked, then the call
+ *    returns KVS_OK without looking at any tensor pointer or the workspace
+ *    (zero-size buffers may be NULL; the varlen calls still need cu_seqlens)
+ *    and without enqueuing work.
  *  - Supported: D in {64, 128}; 1 <= Hkv <= Hq, Hq % Hkv == 0, Hq / Hkv <= 64;
  *    T (max_seqlen) <= 1048576.  Other shapes return KVS_ERR_SHAPE or
  *    KVS_ERR_UNSUPPORTED.

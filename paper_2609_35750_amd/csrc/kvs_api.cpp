@@ -202,17 +202,19 @@ static kvs_status_t fwd_common(const void* Q, const void* K, const void* V, cons
   t_err.clear();
   kvs_status_t st = check_dims(B, T, ntok, Hq, Hkv, D);
   if (st != KVS_OK) return st;
+  if (!(scale > 0.f) || scale != scale) return fail(KVS_ERR_SHAPE, "softmax_scale must be positive and finite");
+  if (flags & ~kKnownFlags) return fail(KVS_ERR_UNSUPPORTED, "unknown flag bits 0x%x", flags & ~kKnownFlags);
+  // An empty batch has nothing to read or write: its pointers (zero-size
+  // buffers, possibly NULL) and workspace are not looked at.
+  if (ntok == 0) return KVS_OK;
   REQUIRE_PTR(Q, "Q");
   REQUIRE_PTR(K, "K");
   REQUIRE_PTR(V, "V");
   REQUIRE_PTR(O, "O");
   REQUIRE_PTR(LSE, "LSE");
   if (!evict_at) return fail(KVS_ERR_NULL, "evict_at is NULL");
-  if (!(scale > 0.f) || scale != scale) return fail(KVS_ERR_SHAPE, "softmax_scale must be positive and finite");
-  if (flags & ~kKnownFlags) return fail(KVS_ERR_UNSUPPORTED, "unknown flag bits 0x%x", flags & ~kKnownFlags);
   st = check_ws(ws, ws_bytes, fwd_ws(B, ntok));
   if (st != KVS_OK) return st;
-  if (ntok == 0) return KVS_OK;
   kvs::Problem p{};
   p.q = Q; p.k = K; p.v = V; p.evict = evict_at; p.cu = cu; p.o = O; p.lse = LSE;
   p.B = B; p.T = T; p.ntok = (int)ntok; p.Hq = Hq; p.Hkv = Hkv; p.D = D; p.G = Hq / Hkv;
@@ -227,6 +229,9 @@ static kvs_status_t bwd_common(const void* dO, const void* Q, const void* K, con
   t_err.clear();
   kvs_status_t st = check_dims(B, T, ntok, Hq, Hkv, D);
   if (st != KVS_OK) return st;
+  if (!(scale > 0.f) || scale != scale) return fail(KVS_ERR_SHAPE, "softmax_scale must be positive and finite");
+  if (flags & ~kKnownFlags) return fail(KVS_ERR_UNSUPPORTED, "unknown flag bits 0x%x", flags & ~kKnownFlags);
+  if (ntok == 0) return KVS_OK;  // empty batch: pointers and workspace are not looked at
   REQUIRE_PTR(dO, "dO");
   REQUIRE_PTR(Q, "Q");
   REQUIRE_PTR(K, "K");
@@ -237,11 +242,8 @@ static kvs_status_t bwd_common(const void* dO, const void* Q, const void* K, con
   REQUIRE_PTR(dK, "dK");
   REQUIRE_PTR(dV, "dV");
   if (!evict_at) return fail(KVS_ERR_NULL, "evict_at is NULL");
-  if (!(scale > 0.f) || scale != scale) return fail(KVS_ERR_SHAPE, "softmax_scale must be positive and finite");
-  if (flags & ~kKnownFlags) return fail(KVS_ERR_UNSUPPORTED, "unknown flag bits 0x%x", flags & ~kKnownFlags);
   st = check_ws(ws, ws_bytes, bwd_ws(B, T, ntok, Hq, Hkv, D));
   if (st != KVS_OK) return st;
-  if (ntok == 0) return KVS_OK;
   kvs::Problem p{};
   p.q = Q; p.k = K; p.v = V; p.o_in = O; p.dout = dO; p.lse_in = LSE; p.evict = evict_at; p.cu = cu;
   p.dq = dQ; p.dk = dK; p.dv = dV;
@@ -325,15 +327,15 @@ kvs_status_t kvs_evict_attn_fwd_noalloc(const void* Q, const void* K, const void
     return fail(KVS_ERR_UNSUPPORTED, "allocation-free forward: %zu bytes of scratch needed, %zu available "
                 "(B + Ntot / 64 + 2 must stay within %zu key tiles)", need, kvs::kNoAllocScratchBytes,
                 kvs::kNoAllocScratchBytes / 8);
+  if (!(softmax_scale > 0.f) || softmax_scale != softmax_scale)
+    return fail(KVS_ERR_SHAPE, "softmax_scale must be positive and finite");
+  if (Ntot == 0) return KVS_OK;  // empty batch: pointers are not looked at
   REQUIRE_PTR(Q, "Q");
   REQUIRE_PTR(K, "K");
   REQUIRE_PTR(V, "V");
   REQUIRE_PTR(O, "O");
   REQUIRE_PTR(LSE, "LSE");
   if (!evict_at) return fail(KVS_ERR_NULL, "evict_at is NULL");
-  if (!(softmax_scale > 0.f) || softmax_scale != softmax_scale)
-    return fail(KVS_ERR_SHAPE, "softmax_scale must be positive and finite");
-  if (Ntot == 0) return KVS_OK;
   void* scratch = nullptr;
   hipError_t e = kvs::noalloc_scratch(&scratch);
   if (e != hipSuccess) return hip_fail(e, "device address of the library scratch");

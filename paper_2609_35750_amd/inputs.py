@@ -60,8 +60,10 @@ def evict_at_layout(L: int, p: int, w: int, s: int, strategy: str = "keep_all") 
     """``evict_at`` (int32, length ``L``) of one trace built from the segment layout."""
     if strategy not in STRATEGIES:
         raise ValueError(f"unknown strategy {strategy!r}")
-    if L < 1 or p < 0 or w < 0 or s < 0:
+    if L < 0 or p < 0 or w < 0 or s < 0:
         raise ValueError("bad layout")
+    if L == 0:  # an empty trace of a varlen batch
+        return np.zeros(0, dtype=np.int32)
     e = np.full(L, L, dtype=np.int64)
     a = segment_starts(L, p, w, s)
     nseg = len(a) - 2

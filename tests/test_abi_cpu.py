@@ -107,6 +107,30 @@ def test_ex_validation(kvs):
     assert kvs.FLAG_NO_EMPTY_SKIP == 1 and kvs.FLAG_FULL_AS_PARTIAL == 2
 
 
+def test_empty_batch_is_a_no_op(kvs):
+    """Ntot = 0 (varlen traces that are all empty) returns OK without looking at any tensor
+    pointer or the workspace, so those may be NULL (cu_seqlens, B + 1 entries, is still required);
+    shapes, scale and flags are still checked.
+    No HIP call happens, so this runs without a GPU."""
+    L = kvs.lib
+    fwd = lambda scale=0.125, Hq=4, D=64: L.kvs_evict_attn_varlen_fwd(
+        None, None, None, None, FAKE, None, None, 3, 0, 1, Hq, 2, D, scale, None, 0, None)
+    assert fwd() == kvs.KVS_OK
+    assert fwd(scale=float("nan")) == kvs.KVS_ERR_SHAPE
+    assert fwd(Hq=3) == kvs.KVS_ERR_SHAPE
+    assert fwd(D=96) == kvs.KVS_ERR_SHAPE
+    st = L.kvs_evict_attn_varlen_bwd(None, None, None, None, None, None, None, FAKE, None, None, None,
+                                     3, 0, 1, 4, 2, 128, 0.1, None, 0, None)
+    assert st == kvs.KVS_OK
+    st = L.kvs_evict_attn_fwd_ex(None, None, None, None, None, None, None, 2, 0, 1, 4, 2, 64, 0.1, 3, None, 0, None)
+    assert st == kvs.KVS_ERR_SHAPE                                  # fixed layout: Ntot = B * max_seqlen
+    st = L.kvs_evict_attn_bwd_ex(None, None, None, None, None, None, None, None, None, None, None,
+                                 2, 0, 1, 4, 2, 64, 0.1, 4, None, 0, None)
+    assert st != kvs.KVS_OK
+    st = L.kvs_evict_attn_fwd_noalloc(None, None, None, None, FAKE, None, None, 2, 0, 1, 4, 2, 64, 0.1, None)
+    assert st == kvs.KVS_OK
+
+
 def test_noalloc_forward_validation(kvs):
     """The allocation-free forward refuses problems beyond its scratch before any HIP call."""
     L = kvs.lib

@@ -138,6 +138,30 @@ def test_varlen_without_prompt(kvs):
 
 
 @pytest.mark.parametrize("D", [128, 64])
+def test_varlen_with_empty_traces(kvs, D):
+    """Empty traces inside the batch, at its start and at its end (a trace whose
+    start is Ntot): every kernel skips them and the others are unaffected."""
+    wl = inputs.custom_workload(f"varlen_empty_D{D}", 6, 2, D, [0, 37, 0, 300, 129, 0], 4, 50, 10, "last2",
+                                varlen=True, seed=15 + D)
+    _parity(kvs, wl, wl.evict_at(), cu=wl.cu_seqlens())
+
+
+def test_empty_batch(kvs):
+    """Ntot = 0: forward and backward return zero-size outputs and enqueue nothing."""
+    dev = torch.device("cuda:0")
+    announce("empty batch Ntot=0")
+    q = torch.empty(0, 4, 64, dtype=torch.bfloat16, device=dev)
+    k = torch.empty(0, 2, 64, dtype=torch.bfloat16, device=dev)
+    ev = torch.empty(0, dtype=torch.int32, device=dev)
+    cu = torch.zeros(3, dtype=torch.int32, device=dev)
+    o, lse = kvs.kvs_evict_attn_fwd(q, k, k, ev, cu_seqlens=cu, max_seqlen=1)
+    assert o.shape == q.shape and lse.shape == (4, 0)
+    dq, dk, dv = kvs.kvs_evict_attn_bwd(q, q, k, k, o, lse, ev, cu_seqlens=cu, max_seqlen=1)
+    assert dq.shape == q.shape and dk.shape == k.shape and dv.shape == k.shape
+    torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("D", [128, 64])
 def test_turn_sliding_window_without_prompt(kvs, D):
     turns = ("sliding_window", 4, 1, 0, 20, 100, 1, 99 + D)
     wl = inputs.custom_workload(f"turns_p0_D{D}", 8, 2, D, [900], 0, 0, 0, seed=98 + D, turns=turns)

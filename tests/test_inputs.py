@@ -25,6 +25,13 @@ def test_latest_only_and_last2_summaries():
     assert (e1[98:100] == 100).all() and (e2[98:100] == 100).all()
 
 
+def test_empty_trace_in_a_varlen_batch():
+    wl = inputs.custom_workload("e", 4, 2, 64, [0, 9, 0], 2, 3, 1, "last2", varlen=True)
+    assert wl.ntok == 9 and list(wl.cu_seqlens()) == [0, 0, 9, 9]
+    np.testing.assert_array_equal(wl.evict_at(), inputs.evict_at_layout(9, 2, 3, 1, "last2"))
+    assert inputs.evict_at_layout(0, 2, 3, 1).shape == (0,)
+
+
 def test_workload_sizes():
     W = inputs.WORKLOADS
     assert W["trace16k_gqa4"].ntok == 16384 and W["trace16k_gqa4"].G == 4
