@@ -29,6 +29,9 @@ and for the scalar loss sum(dO * O):
 The mask is built explicitly as a boolean matrix; the softmax is two-pass
 (row max, then sum) over the full causal prefix of each block of query rows.
 Nothing is skipped.  Inputs are the exact bf16 values widened to fp64.
+For traces too long for that, ``rows_reference`` and ``keys_reference``
+evaluate the same definitions at chosen rows or keys, each row over its
+visible set V(i) gathered from ``evict_at``.
 
 Parity of every function here is pinned by tests against causal attention
 (``e = inf``), a brute-force stream replay, finite differences, closed forms
@@ -283,3 +286,109 @@ def dkdv_rounding_rss(q, k, v, evict_at, scale, do, cu_seqlens=None):
                 SV2[a:a + i1, g, :] += (P ** 2).T @ (do[a + i0:a + i1, h, :] ** 2)
                 SK2[a:a + i1, g, :] += (dS ** 2 + P ** 2 * R2).T @ (q[a + i0:a + i1, h, :] ** 2)
     return scale * np.sqrt(SK2), np.sqrt(SV2)
+
+
+def _visible_keys(e_tr: np.ndarray, L: int, i: int) -> np.ndarray:
+    """Trace-local keys of V(i) = { j <= i : i < min(e_j, L) }, ascending."""
+    return np.nonzero(np.minimum(e_tr[:i + 1], L) > i)[0]
+
+
+def _row_terms(q_row, do_row, kv, vv, scale):
+    """One query row and one q-head over the keys of its visible set (rows of kv, vv):
+    P, dP, Delta, dS and O of the definitions in the module docstring, and LSE."""
+    s = scale * (kv @ q_row)
+    m = s.max()
+    ex = np.exp(s - m)
+    l = ex.sum()
+    P = ex / l
+    O = P @ vv
+    dP = vv @ do_row
+    dlt = P @ dP
+    dS = P * (dP - dlt)
+    return P, dS, O, m + np.log(l), dlt
+
+
+def _trace_of(pos: int, cu_seqlens, n: int):
+    for a, b in _split(cu_seqlens, n):
+        if a <= pos < b:
+            return a, b
+    raise ValueError(f"position {pos} outside [0, {n})")
+
+
+def rows_reference(q, k, v, evict_at, scale, do, rows, cu_seqlens=None):
+    """O, LSE, Delta, dQ and the dQ rounding sensitivity E at the packed query rows ``rows`` only.
+
+    Each row's quantities depend on its own visible set V(i) alone, so they are
+    computed from that set (gathered from ``evict_at``) instead of the full
+    causal prefix: the same definitions as ``backward`` and
+    ``dq_rounding_scale`` at any trace length.  Only the gathered rows and keys
+    are widened to fp64.  Returns fp64 ``O, dq, E [len(rows), Hq, D]`` and
+    ``LSE, Delta [Hq, len(rows)]``.
+    """
+    e = np.asarray(evict_at, dtype=np.int64)
+    rows = np.asarray(rows, dtype=np.int64)
+    n, Hq, D = q.shape
+    G = Hq // k.shape[1]
+    out = {"O": np.zeros((rows.size, Hq, D)), "dq": np.zeros((rows.size, Hq, D)), "E": np.zeros((rows.size, Hq, D)),
+           "LSE": np.zeros((Hq, rows.size)), "Delta": np.zeros((Hq, rows.size))}
+    for r, pos in enumerate(rows):
+        a, b = _trace_of(int(pos), cu_seqlens, n)
+        L = b - a
+        js = a + _visible_keys(e[a:b], L, int(pos) - a)
+        for h in range(Hq):
+            g = h // G
+            kv, vv = _f64(k[js, g]), _f64(v[js, g])
+            do_row = _f64(do[pos, h])
+            P, dS, O, lse, dlt = _row_terms(_f64(q[pos, h]), do_row, kv, vv, scale)
+            out["O"][r, h], out["LSE"][h, r], out["Delta"][h, r] = O, lse, dlt
+            out["dq"][r, h] = scale * (dS @ kv)
+            R = np.abs(do_row) @ np.abs(O)
+            out["E"][r, h] = scale * (np.abs(dS) @ np.abs(kv) + np.abs(P @ kv) * R)
+    return out
+
+
+def keys_reference(q, k, v, evict_at, scale, do, keys, cu_seqlens=None):
+    """dK and dV at the packed keys ``keys`` only.
+
+    Key j of a trace is seen by the rows R(j) = [j, min(e_j, L)).  The union
+    of those rows is processed once, in blocks of consecutive rows as in
+    ``backward``, but each block's columns are only the keys some row of the
+    block can see (j <= the block's last row, min(e_j, L) > its first), with
+    the explicit mask on top: every row's P and dS, so its LSE and Delta, are
+    those of the definition.  Returns fp64 ``dk, dv [len(keys), Hkv, D]``.
+    """
+    e = np.asarray(evict_at, dtype=np.int64)
+    keys = np.asarray(keys, dtype=np.int64)
+    n, Hq, D = q.shape
+    Hkv = k.shape[1]
+    G = Hq // Hkv
+    dk = np.zeros((keys.size, Hkv, D))
+    dv = np.zeros((keys.size, Hkv, D))
+    for a, b in _split(cu_seqlens, n):
+        L = b - a
+        mine = np.nonzero((keys >= a) & (keys < b))[0]
+        if mine.size == 0:
+            continue
+        et = np.minimum(e[a:b], L)
+        rows = np.unique(np.concatenate([np.arange(keys[c] - a, et[keys[c] - a]) for c in mine]))
+        for c0 in range(0, rows.size, ROW_BLOCK):
+            il = rows[c0:c0 + ROW_BLOCK]
+            cand = np.nonzero(et[:il[-1] + 1] > il[0])[0]          # keys some row of the block may see
+            M = (cand[None, :] <= il[:, None]) & (il[:, None] < et[cand][None, :])
+            pos = {int(j): t for t, j in enumerate(cand)}
+            cols = [(c, pos[int(keys[c] - a)]) for c in mine if int(keys[c] - a) in pos]
+            if not cols:
+                continue
+            for h in range(Hq):
+                g = h // G
+                qb, dob = _f64(q[a + il, h]), _f64(do[a + il, h])
+                kc, vc = _f64(k[a + cand, g]), _f64(v[a + cand, g])
+                S = np.where(M, scale * (qb @ kc.T), -np.inf)
+                E = np.where(M, np.exp(S - S.max(axis=1, keepdims=True)), 0.0)
+                P = E / E.sum(axis=1, keepdims=True)
+                dP = dob @ vc.T
+                dS = P * (dP - (P * dP).sum(axis=1, keepdims=True))
+                for c, t in cols:
+                    dv[c, g] += P[:, t] @ dob
+                    dk[c, g] += scale * (dS[:, t] @ qb)
+    return dk, dv

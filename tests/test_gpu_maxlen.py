@@ -1,0 +1,96 @@
+"""The longest trace the library accepts: 2^20 tokens, the sequence-length limit
+of the C ABI, in one call (fixed layout, B = 1).
+
+At this length the key blocks of the prompt stay visible to every one of
+16,384 row-steps, more than the split slots of the dK/dV plan can take, so
+some of them run as single long work items; the row kernels' tile walkers
+skip thousands of empty key tiles per row block; every grid, workspace and
+offset is at its largest for one trace.  The expected values come from the
+fp64 checker evaluated at sampled rows and keys only (each row over its own
+visible set: ``oracle.attention.rows_reference`` / ``keys_reference``); keys
+that every row sees (the prompt) are outside what it can sum in a test's
+time and are covered by the whole-tensor finiteness check and by the
+bit-identical tile-classifier switches.  Bounds as in the other parity
+tests (tests/gpu_helpers.py).
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import attention as orc
+from paper_2609_35750_amd import inputs
+from tests.gpu_helpers import announce, assert_close, assert_lse, to_f64
+
+pytestmark = pytest.mark.gpu
+
+L_MAX = 1 << 20
+
+
+@pytest.fixture(scope="module")
+def kvs():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_35750_amd import kvs as k
+
+    return k
+
+
+def _sample_rows(L, p, starts, rng):
+    marks = {0, 1, p - 1, p, L // 2, L - 2, L - 1}
+    for a in (starts[1], starts[len(starts) // 2], starts[-3]):
+        marks |= {a - 1, a, a + 1}
+    marks |= set(rng.integers(0, L, 24).tolist())
+    return np.array(sorted(m for m in marks if 0 <= m < L), dtype=np.int64)
+
+
+def _sample_keys(L, p, w, starts):
+    """Keys past the prompt: segment starts and ends, summaries, the trace end."""
+    out = set()
+    for a in (starts[1], starts[len(starts) // 2], starts[-3]):
+        out |= {a, a + 1, a + w - 1, a + w, a + w + 1}
+    out |= {L - 700, L - 2, L - 1}
+    return np.array(sorted(j for j in out if p <= j < L), dtype=np.int64)
+
+
+def test_maximum_sequence_length(kvs):
+    p, w, s = 2048, 1024, 128
+    wl = inputs.custom_workload("maxlen_2p20", 4, 2, 128, [L_MAX], p, w, s, "latest_only", seed=20)
+    announce(f"maximum trace length: tokens={L_MAX} Hq={wl.Hq} Hkv={wl.Hkv} D={wl.D} latest_only p={p} w={w} s={s}")
+    e = wl.evict_at()
+    t = inputs.make_tensors(wl)
+    dev = torch.device("cuda:0")
+    shp = lambda x: x.to(dev).view(1, L_MAX, x.shape[1], wl.D)
+    q, k, v, do = (shp(t[x]) for x in ("q", "k", "v", "do"))
+    ev = torch.from_numpy(e).to(dev).view(1, L_MAX)
+
+    def run(flags=0):
+        o, lse = kvs.kvs_evict_attn_fwd(q, k, v, ev, wl.softmax_scale, flags=flags)
+        dq, dk, dv = kvs.kvs_evict_attn_bwd(do, q, k, v, o, lse, ev, wl.softmax_scale, flags=flags)
+        torch.cuda.synchronize()
+        return {"O": o[0], "LSE": lse[0], "dq": dq[0], "dk": dk[0], "dv": dv[0]}
+
+    res = run()
+    for key, x in res.items():
+        assert torch.isfinite(x.float()).all(), f"non-finite {key}"
+    for flags in (kvs.FLAG_NO_EMPTY_SKIP, kvs.FLAG_FULL_AS_PARTIAL):
+        other = run(flags)
+        for key in res:
+            a, b = res[key], other[key]
+            if a.dtype == torch.bfloat16:
+                a, b = a.view(torch.int16), b.view(torch.int16)
+            assert torch.equal(a, b), f"{key} differs bitwise with flags {flags}"
+        del other
+    print("[bitwise] 2^20 tokens: switches give identical O, LSE, dQ, dK, dV", flush=True)
+
+    starts = inputs.segment_starts(L_MAX, p, w, s)
+    rows = _sample_rows(L_MAX, p, starts, np.random.default_rng(21))
+    keys = _sample_keys(L_MAX, p, w, starts)
+    ref = orc.rows_reference(t["q"], t["k"], t["v"], e, wl.softmax_scale, t["do"], rows)
+    rows_t = torch.from_numpy(rows).to(dev)
+    assert_close("maxlen:O", to_f64(res["O"].index_select(0, rows_t)), ref["O"])
+    assert_close("maxlen:dQ", to_f64(res["dq"].index_select(0, rows_t)), ref["dq"], E=ref["E"])
+    assert_lse("maxlen", to_f64(res["LSE"].index_select(1, rows_t)), ref["LSE"])
+    dk_ref, dv_ref = orc.keys_reference(t["q"], t["k"], t["v"], e, wl.softmax_scale, t["do"], keys)
+    keys_t = torch.from_numpy(keys).to(dev)
+    assert_close("maxlen:dK", to_f64(res["dk"].index_select(0, keys_t)), dk_ref)
+    assert_close("maxlen:dV", to_f64(res["dv"].index_select(0, keys_t)), dv_ref)

@@ -30,6 +30,11 @@ MUTATIONS = {
     "forward unscaled": ("            S = scale * (q[i0:i1, h, :] @ k[:i1, g, :].T)\n            S = np.where(M, S, -np.inf)\n            m = S.max(axis=1, keepdims=True)\n            E = np.where(M, np.exp(S - m), 0.0)\n            l = E.sum(axis=1, keepdims=True)\n            P = E / l\n            O[i0:i1, h, :] = P @ v[:i1, g, :]\n            LSE[h, i0:i1] = (m + np.log(l))[:, 0]\n    return O, LSE",
                          "            S = q[i0:i1, h, :] @ k[:i1, g, :].T\n            S = np.where(M, S, -np.inf)\n            m = S.max(axis=1, keepdims=True)\n            E = np.where(M, np.exp(S - m), 0.0)\n            l = E.sum(axis=1, keepdims=True)\n            P = E / l\n            O[i0:i1, h, :] = P @ v[:i1, g, :]\n            LSE[h, i0:i1] = (m + np.log(l))[:, 0]\n    return O, LSE"),
     "eviction index ignored": ("ej = np.minimum(e[:j1].astype(np.int64), L)[None, :]", "ej = np.full((1, j1), L)"),
+    "sampled rows: diagonal excluded": ("np.minimum(e_tr[:i + 1], L) > i", "np.minimum(e_tr[:i], L) > i"),
+    "sampled keys: rows past the eviction": ("(il[:, None] < et[cand][None, :])", "(il[:, None] <= et[cand][None, :])"),
+    "sampled rows: dQ without scale": ('out["dq"][r, h] = scale * (dS @ kv)', 'out["dq"][r, h] = dS @ kv'),
+    "sampled keys: dK without scale": ("dk[c, g] += scale * (dS[:, t] @ qb)", "dk[c, g] += dS[:, t] @ qb"),
+    "sampled keys: dV from dS": ("dv[c, g] += P[:, t] @ dob", "dv[c, g] += dS[:, t] @ dob"),
 }
 
 
@@ -72,6 +77,15 @@ def _pins(orc):
     np.testing.assert_allclose(res["LSE"], LSE.detach().numpy(), rtol=1e-10, atol=1e-10)
     for key, g in (("dq", qt.grad), ("dk", kt.grad), ("dv", vt.grad)):
         np.testing.assert_allclose(res[key], g.numpy(), rtol=1e-9, atol=1e-10)
+    # the row- and key-sampled forms against the same replay
+    pos = np.arange(L)
+    rr = orc.rows_reference(q, k, v, e, scale, do, pos)
+    np.testing.assert_allclose(rr["O"], O.detach().numpy(), rtol=1e-10, atol=1e-10)
+    np.testing.assert_allclose(rr["LSE"], LSE.detach().numpy(), rtol=1e-10, atol=1e-10)
+    np.testing.assert_allclose(rr["dq"], qt.grad.numpy(), rtol=1e-9, atol=1e-10)
+    sk, sv = orc.keys_reference(q, k, v, e, scale, do, pos)
+    np.testing.assert_allclose(sk, kt.grad.numpy(), rtol=1e-9, atol=1e-10)
+    np.testing.assert_allclose(sv, vt.grad.numpy(), rtol=1e-9, atol=1e-10)
 
 
 def test_unmutated_checker_passes_battery():

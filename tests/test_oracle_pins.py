@@ -268,6 +268,56 @@ def test_varlen_is_concatenation():
         np.testing.assert_array_equal(res["LSE"][:, a:z], one["LSE"])
 
 
+# ---------------------------------------------------------------- row- and key-sampled forms (long traces)
+def test_sampled_forms_match_replay_and_closed_forms():
+    """``rows_reference`` / ``keys_reference`` (each row from its own visible set)
+    against the token-by-token replay of the compacted stream, with gradients,
+    and against the self-only closed form; packed traces with an empty one
+    match the per-trace values."""
+    L, p, w, s_, Hq, Hkv, D = 70, 4, 12, 3, 4, 2, 8
+    scale = 1 / math.sqrt(D)
+    e = inputs.evict_at_layout(L, p, w, s_, "last2")
+    q, k, v, do = _rand((L, Hq, D), 71), _rand((L, Hkv, D), 72), _rand((L, Hkv, D), 73), _rand((L, Hq, D), 74)
+    qt, kt, vt = (x.double().clone().requires_grad_(True) for x in (q, k, v))
+    O, LSE = stream_sim.replay(qt, kt, vt, p, w, s_, "last2", scale)
+    (O * do.double()).sum().backward()
+    pos = np.arange(L)
+    rr = orc.rows_reference(q, k, v, e, scale, do, pos[::-1])
+    np.testing.assert_allclose(rr["O"], O.detach().numpy()[::-1], rtol=1e-10, atol=1e-10)
+    np.testing.assert_allclose(rr["LSE"], LSE.detach().numpy()[:, ::-1], rtol=1e-10, atol=1e-10)
+    np.testing.assert_allclose(rr["dq"], qt.grad.numpy()[::-1], rtol=1e-9, atol=1e-10)
+    dk, dv = orc.keys_reference(q, k, v, e, scale, do, pos)
+    np.testing.assert_allclose(dk, kt.grad.numpy(), rtol=1e-9, atol=1e-10)
+    np.testing.assert_allclose(dv, vt.grad.numpy(), rtol=1e-9, atol=1e-10)
+    # self only (e_j = j + 1): O_i = v_i, LSE_i = s_ii, dQ = dK = 0, dV_j = sum over the group of dO_j
+    e1 = np.arange(1, L + 1)
+    rr = orc.rows_reference(q, k, v, e1, scale, do, pos)
+    G = Hq // Hkv
+    vq = v.double().numpy().repeat(G, axis=1)
+    np.testing.assert_allclose(rr["O"], vq, rtol=0, atol=1e-15)
+    s_ii = scale * (q.double().numpy() * k.double().numpy().repeat(G, axis=1)).sum(-1).T
+    np.testing.assert_allclose(rr["LSE"], s_ii, rtol=1e-14, atol=1e-14)
+    assert np.abs(rr["dq"]).max() == 0.0
+    dk, dv = orc.keys_reference(q, k, v, e1, scale, do, pos)
+    assert np.abs(dk).max() == 0.0
+    np.testing.assert_allclose(dv, do.double().numpy().reshape(L, Hkv, G, D).sum(2), rtol=1e-15, atol=0)
+    # packed traces, one empty: every row and key as in its own trace, E as dq_rounding_scale gives it
+    lengths = [21, 0, 33, 9]
+    n = sum(lengths)
+    rng = np.random.default_rng(5)
+    ep = np.concatenate([inputs.evict_at_random(x, rng) for x in lengths if x])
+    cu = np.concatenate([[0], np.cumsum(lengths)])
+    q, k, v, do = _rand((n, Hq, D), 75), _rand((n, Hkv, D), 76), _rand((n, Hkv, D), 77), _rand((n, Hq, D), 78)
+    full = orc.backward(q, k, v, ep, 0.4, do, cu_seqlens=cu)
+    E = orc.dq_rounding_scale(q, k, v, ep, 0.4, do, np.arange(n), cu_seqlens=cu)
+    rr = orc.rows_reference(q, k, v, ep, 0.4, do, np.arange(n), cu_seqlens=cu)
+    for key, want in (("O", full["O"]), ("dq", full["dq"]), ("E", E), ("LSE", full["LSE"]), ("Delta", full["Delta"])):
+        np.testing.assert_allclose(rr[key], want, rtol=1e-12, atol=1e-13)
+    dk, dv = orc.keys_reference(q, k, v, ep, 0.4, do, np.arange(n), cu_seqlens=cu)
+    np.testing.assert_allclose(dk, full["dk"], rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(dv, full["dv"], rtol=1e-12, atol=1e-13)
+
+
 def test_invalid_evict_at_rejected():
     q = _rand((5, 1, 8), 1)
     with pytest.raises(ValueError):
