@@ -177,6 +177,17 @@ def test_varlen_many_short_traces(kvs):
     _parity(kvs, wl, wl.evict_at(), cu=wl.cu_seqlens())
 
 
+def test_varlen_600_traces(kvs):
+    """600 packed traces of 0-300 tokens: more traces than the dK/dV plan groups
+    by trace (it then orders work items by length alone), trace indices in the
+    hundreds in every kernel's addressing, and empty traces among them."""
+    rng = np.random.default_rng(600)
+    lengths = [int(x) for x in rng.integers(0, 301, 600)]
+    wl = inputs.custom_workload("varlen_600", 4, 2, 128, lengths, 16, 60, 12, "last2", varlen=True, seed=600)
+    assert wl.B > 256 and 0 in lengths
+    _parity(kvs, wl, wl.evict_at(), cu=wl.cu_seqlens())
+
+
 # Traces past 8192 rows have key blocks (the prompt) visible to more than two
 # 4096-row chunks: the dK/dV work is then split into row chunks whose fp32
 # partial sums are added afterwards.  Element-by-element parity and bitwise
