@@ -288,24 +288,28 @@ def dkdv_rounding_rss(q, k, v, evict_at, scale, do, cu_seqlens=None):
     return scale * np.sqrt(SK2), np.sqrt(SV2)
 
 
+def _gatherable(x):
+    """A numpy array to gather rows from without widening the whole tensor: the
+    raw 16-bit patterns of a bf16 torch tensor (no copy), else fp64."""
+    if hasattr(x, "detach"):
+        import torch
+
+        if x.dtype == torch.bfloat16:
+            return x.detach().cpu().contiguous().view(torch.int16).numpy()
+    return _f64(x)
+
+
+def _widen(a: np.ndarray) -> np.ndarray:
+    """fp64 values of gathered elements: bf16 bit patterns become the fp32 with
+    those upper 16 bits (exact), widened to fp64; floats are widened."""
+    if a.dtype == np.int16:
+        return (a.astype(np.int32) << 16).view(np.float32).astype(np.float64)
+    return np.asarray(a, dtype=np.float64)
+
+
 def _visible_keys(e_tr: np.ndarray, L: int, i: int) -> np.ndarray:
     """Trace-local keys of V(i) = { j <= i : i < min(e_j, L) }, ascending."""
     return np.nonzero(np.minimum(e_tr[:i + 1], L) > i)[0]
-
-
-def _row_terms(q_row, do_row, kv, vv, scale):
-    """One query row and one q-head over the keys of its visible set (rows of kv, vv):
-    P, dP, Delta, dS and O of the definitions in the module docstring, and LSE."""
-    s = scale * (kv @ q_row)
-    m = s.max()
-    ex = np.exp(s - m)
-    l = ex.sum()
-    P = ex / l
-    O = P @ vv
-    dP = vv @ do_row
-    dlt = P @ dP
-    dS = P * (dP - dlt)
-    return P, dS, O, m + np.log(l), dlt
 
 
 def _trace_of(pos: int, cu_seqlens, n: int):
@@ -320,30 +324,39 @@ def rows_reference(q, k, v, evict_at, scale, do, rows, cu_seqlens=None):
 
     Each row's quantities depend on its own visible set V(i) alone, so they are
     computed from that set (gathered from ``evict_at``) instead of the full
-    causal prefix: the same definitions as ``backward`` and
-    ``dq_rounding_scale`` at any trace length.  Only the gathered rows and keys
-    are widened to fp64.  Returns fp64 ``O, dq, E [len(rows), Hq, D]`` and
-    ``LSE, Delta [Hq, len(rows)]``.
+    causal prefix, for the G q-heads of a KV head together: the same
+    definitions as ``backward`` and ``dq_rounding_scale`` at any trace length.
+    Only the gathered rows and keys are widened to fp64.  Returns fp64
+    ``O, dq, E [len(rows), Hq, D]`` and ``LSE, Delta [Hq, len(rows)]``.
     """
     e = np.asarray(evict_at, dtype=np.int64)
     rows = np.asarray(rows, dtype=np.int64)
     n, Hq, D = q.shape
-    G = Hq // k.shape[1]
+    Hkv = k.shape[1]
+    G = Hq // Hkv
     out = {"O": np.zeros((rows.size, Hq, D)), "dq": np.zeros((rows.size, Hq, D)), "E": np.zeros((rows.size, Hq, D)),
            "LSE": np.zeros((Hq, rows.size)), "Delta": np.zeros((Hq, rows.size))}
+    qr, kr, vr, dor = (_gatherable(x) for x in (q, k, v, do))
     for r, pos in enumerate(rows):
         a, b = _trace_of(int(pos), cu_seqlens, n)
-        L = b - a
-        js = a + _visible_keys(e[a:b], L, int(pos) - a)
-        for h in range(Hq):
-            g = h // G
-            kv, vv = _f64(k[js, g]), _f64(v[js, g])
-            do_row = _f64(do[pos, h])
-            P, dS, O, lse, dlt = _row_terms(_f64(q[pos, h]), do_row, kv, vv, scale)
-            out["O"][r, h], out["LSE"][h, r], out["Delta"][h, r] = O, lse, dlt
-            out["dq"][r, h] = scale * (dS @ kv)
-            R = np.abs(do_row) @ np.abs(O)
-            out["E"][r, h] = scale * (np.abs(dS) @ np.abs(kv) + np.abs(P @ kv) * R)
+        js = a + _visible_keys(e[a:b], b - a, int(pos) - a)
+        for g in range(Hkv):
+            hs = slice(g * G, (g + 1) * G)
+            kv, vv = _widen(kr[js, g]), _widen(vr[js, g])          # [|V(i)|, D]
+            qg, dog = _widen(qr[pos, hs]), _widen(dor[pos, hs])    # [G, D]
+            S = scale * (qg @ kv.T)
+            m = S.max(axis=1, keepdims=True)
+            ex = np.exp(S - m)
+            l = ex.sum(axis=1, keepdims=True)
+            P = ex / l
+            O = P @ vv
+            dP = dog @ vv.T
+            dlt = (P * dP).sum(axis=1, keepdims=True)
+            dS = P * (dP - dlt)
+            out["O"][r, hs], out["LSE"][hs, r], out["Delta"][hs, r] = O, (m + np.log(l))[:, 0], dlt[:, 0]
+            out["dq"][r, hs] = scale * (dS @ kv)
+            R = (np.abs(dog) * np.abs(O)).sum(axis=1, keepdims=True)
+            out["E"][r, hs] = scale * (np.abs(dS) @ np.abs(kv) + np.abs(P @ kv) * R)
     return out
 
 
@@ -352,10 +365,11 @@ def keys_reference(q, k, v, evict_at, scale, do, keys, cu_seqlens=None):
 
     Key j of a trace is seen by the rows R(j) = [j, min(e_j, L)).  The union
     of those rows is processed once, in blocks of consecutive rows as in
-    ``backward``, but each block's columns are only the keys some row of the
+    ``backward`` (no block spans a gap), but each block's columns are only the keys some row of the
     block can see (j <= the block's last row, min(e_j, L) > its first), with
     the explicit mask on top: every row's P and dS, so its LSE and Delta, are
-    those of the definition.  Returns fp64 ``dk, dv [len(keys), Hkv, D]``.
+    those of the definition.  The G q-heads of a KV head are stacked as extra
+    rows.  Returns fp64 ``dk, dv [len(keys), Hkv, D]``.
     """
     e = np.asarray(evict_at, dtype=np.int64)
     keys = np.asarray(keys, dtype=np.int64)
@@ -364,6 +378,7 @@ def keys_reference(q, k, v, evict_at, scale, do, keys, cu_seqlens=None):
     G = Hq // Hkv
     dk = np.zeros((keys.size, Hkv, D))
     dv = np.zeros((keys.size, Hkv, D))
+    qr, kr, vr, dor = (_gatherable(x) for x in (q, k, v, do))
     for a, b in _split(cu_seqlens, n):
         L = b - a
         mine = np.nonzero((keys >= a) & (keys < b))[0]
@@ -371,18 +386,21 @@ def keys_reference(q, k, v, evict_at, scale, do, keys, cu_seqlens=None):
             continue
         et = np.minimum(e[a:b], L)
         rows = np.unique(np.concatenate([np.arange(keys[c] - a, et[keys[c] - a]) for c in mine]))
-        for c0 in range(0, rows.size, ROW_BLOCK):
-            il = rows[c0:c0 + ROW_BLOCK]
+        runs = np.split(rows, np.nonzero(np.diff(rows) > 1)[0] + 1)   # consecutive rows
+        blocks = [r[c0:c0 + ROW_BLOCK] for r in runs for c0 in range(0, r.size, ROW_BLOCK)]
+        for il in blocks:
             cand = np.nonzero(et[:il[-1] + 1] > il[0])[0]          # keys some row of the block may see
             M = (cand[None, :] <= il[:, None]) & (il[:, None] < et[cand][None, :])
+            M = np.repeat(M, G, axis=0)                           # rows (i, h) with h the fast index
             pos = {int(j): t for t, j in enumerate(cand)}
             cols = [(c, pos[int(keys[c] - a)]) for c in mine if int(keys[c] - a) in pos]
             if not cols:
                 continue
-            for h in range(Hq):
-                g = h // G
-                qb, dob = _f64(q[a + il, h]), _f64(do[a + il, h])
-                kc, vc = _f64(k[a + cand, g]), _f64(v[a + cand, g])
+            for g in range(Hkv):
+                hs = slice(g * G, (g + 1) * G)
+                qb = _widen(qr[a + il, hs]).reshape(-1, D)
+                dob = _widen(dor[a + il, hs]).reshape(-1, D)
+                kc, vc = _widen(kr[a + cand, g]), _widen(vr[a + cand, g])
                 S = np.where(M, scale * (qb @ kc.T), -np.inf)
                 E = np.where(M, np.exp(S - S.max(axis=1, keepdims=True)), 0.0)
                 P = E / E.sum(axis=1, keepdims=True)

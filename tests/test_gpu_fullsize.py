@@ -23,6 +23,7 @@ import numpy as np
 import pytest
 import torch
 
+from oracle import attention as orc
 from paper_2609_35750_amd import inputs
 from tests.gpu_helpers import REL_L2, announce, assert_close, assert_lse, to_f64
 
@@ -115,3 +116,40 @@ def test_fullsize_tile_shortcuts_are_exact(kvs, name):
             assert torch.equal(a, b), f"{name}: {key} differs bitwise with flags {flags}"
         del other
         print(f"[bitwise] {name}: flags {flags}: O, LSE, dQ, dK, dV identical over the whole tensors", flush=True)
+
+
+@pytest.mark.parametrize("name", NAMES)
+def test_fullsize_every_head_sampled(kvs, name):
+    """Every q-head and every KV head at the benchmarked launch configuration:
+    O, LSE and dQ at the fixture's sampled rows for all q-heads, and dK, dV for
+    all KV heads at the sampled keys seen by the fewest rows, against the
+    checker's row- and key-sampled forms evaluated here."""
+    path = os.path.join(GOLDEN, f"parity_{name}.npz")
+    if not os.path.exists(path):
+        pytest.skip(f"{path} not generated")
+    gold = np.load(path)
+    wl = inputs.WORKLOADS[name]
+    announce(f"full-size every head {name}: tokens={wl.ntok} Hq={wl.Hq} Hkv={wl.Hkv}")
+    t = inputs.make_tensors(wl)
+    e = wl.evict_at()
+    cu = wl.cu_seqlens() if wl.varlen else None
+    res = _run(kvs, wl, _device_inputs(wl))
+    rows = gold["rows"]
+    ref = orc.rows_reference(t["q"], t["k"], t["v"], e, wl.softmax_scale, t["do"], rows, cu_seqlens=cu)
+    rows_t = torch.from_numpy(rows).cuda()
+    assert_close(f"{name}:O all heads", to_f64(res["O"].index_select(0, rows_t)), ref["O"])
+    assert_close(f"{name}:dQ all heads", to_f64(res["dq"].index_select(0, rows_t)), ref["dq"], E=ref["E"])
+    assert_lse(f"{name} all heads", to_f64(res["LSE"].index_select(1, rows_t)), ref["LSE"])
+    # keys: the 8 sampled keys with the fewest rows that see them (their sums stay cheap for every head)
+    keys = gold["keys"]
+    span = np.empty(keys.size, dtype=np.int64)
+    for c, j in enumerate(keys):
+        a = int(np.searchsorted(cu, j, side="right")) - 1 if cu is not None else 0
+        start = int(cu[a]) if cu is not None else 0
+        L = int(cu[a + 1] - cu[a]) if cu is not None else wl.ntok
+        span[c] = min(int(e[j]), L) - (int(j) - start)
+    pick = np.sort(keys[np.argsort(span, kind="stable")[:8]])
+    dk_ref, dv_ref = orc.keys_reference(t["q"], t["k"], t["v"], e, wl.softmax_scale, t["do"], pick, cu_seqlens=cu)
+    keys_t = torch.from_numpy(pick).cuda()
+    assert_close(f"{name}:dK all KV heads", to_f64(res["dk"].index_select(0, keys_t)), dk_ref)
+    assert_close(f"{name}:dV all KV heads", to_f64(res["dv"].index_select(0, keys_t)), dv_ref)

@@ -32,7 +32,7 @@ MUTATIONS = {
     "eviction index ignored": ("ej = np.minimum(e[:j1].astype(np.int64), L)[None, :]", "ej = np.full((1, j1), L)"),
     "sampled rows: diagonal excluded": ("np.minimum(e_tr[:i + 1], L) > i", "np.minimum(e_tr[:i], L) > i"),
     "sampled keys: rows past the eviction": ("(il[:, None] < et[cand][None, :])", "(il[:, None] <= et[cand][None, :])"),
-    "sampled rows: dQ without scale": ('out["dq"][r, h] = scale * (dS @ kv)', 'out["dq"][r, h] = dS @ kv'),
+    "sampled rows: dQ without scale": ('out["dq"][r, hs] = scale * (dS @ kv)', 'out["dq"][r, hs] = dS @ kv'),
     "sampled keys: dK without scale": ("dk[c, g] += scale * (dS[:, t] @ qb)", "dk[c, g] += dS[:, t] @ qb"),
     "sampled keys: dV from dS": ("dv[c, g] += P[:, t] @ dob", "dv[c, g] += dS[:, t] @ dob"),
 }
