@@ -118,6 +118,17 @@ def test_fullsize_tile_shortcuts_are_exact(kvs, name):
         print(f"[bitwise] {name}: flags {flags}: O, LSE, dQ, dK, dV identical over the whole tensors", flush=True)
 
 
+def _fewest_rows_keys(keys, e, cu, ntok, count=8):
+    """The ``count`` sampled keys seen by the fewest rows (their sums stay cheap for every head)."""
+    span = np.empty(keys.size, dtype=np.int64)
+    for c, j in enumerate(keys):
+        b = int(np.searchsorted(cu, j, side="right")) - 1 if cu is not None else 0
+        start = int(cu[b]) if cu is not None else 0
+        L = int(cu[b + 1] - cu[b]) if cu is not None else ntok
+        span[c] = min(int(e[j]), L) - (int(j) - start)
+    return np.sort(keys[np.argsort(span, kind="stable")[:count]])
+
+
 @pytest.mark.parametrize("name", NAMES)
 def test_fullsize_every_head_sampled(kvs, name):
     """Every q-head and every KV head at the benchmarked launch configuration:
@@ -140,16 +151,47 @@ def test_fullsize_every_head_sampled(kvs, name):
     assert_close(f"{name}:O all heads", to_f64(res["O"].index_select(0, rows_t)), ref["O"])
     assert_close(f"{name}:dQ all heads", to_f64(res["dq"].index_select(0, rows_t)), ref["dq"], E=ref["E"])
     assert_lse(f"{name} all heads", to_f64(res["LSE"].index_select(1, rows_t)), ref["LSE"])
-    # keys: the 8 sampled keys with the fewest rows that see them (their sums stay cheap for every head)
-    keys = gold["keys"]
-    span = np.empty(keys.size, dtype=np.int64)
-    for c, j in enumerate(keys):
-        a = int(np.searchsorted(cu, j, side="right")) - 1 if cu is not None else 0
-        start = int(cu[a]) if cu is not None else 0
-        L = int(cu[a + 1] - cu[a]) if cu is not None else wl.ntok
-        span[c] = min(int(e[j]), L) - (int(j) - start)
-    pick = np.sort(keys[np.argsort(span, kind="stable")[:8]])
+    pick = _fewest_rows_keys(gold["keys"], e, cu, wl.ntok)
     dk_ref, dv_ref = orc.keys_reference(t["q"], t["k"], t["v"], e, wl.softmax_scale, t["do"], pick, cu_seqlens=cu)
     keys_t = torch.from_numpy(pick).cuda()
     assert_close(f"{name}:dK all KV heads", to_f64(res["dk"].index_select(0, keys_t)), dk_ref)
     assert_close(f"{name}:dV all KV heads", to_f64(res["dv"].index_select(0, keys_t)), dv_ref)
+
+
+@pytest.mark.parametrize("name", ["trace16k_gqa4", "varlen8_gqa5"])
+def test_fullsize_head_dim_64(kvs, name):
+    """The D = 64 kernels at full size (same layouts, head dimension 64): every
+    q-head at the fixture's sampled rows, every KV head at the sampled keys
+    seen by the fewest rows, against the sampled checker; finiteness and the
+    tile-classifier switches bit for bit over the whole tensors."""
+    import dataclasses
+
+    gold = np.load(os.path.join(GOLDEN, f"parity_{name}.npz"))
+    wl = dataclasses.replace(inputs.WORKLOADS[name], D=64)
+    announce(f"full-size D=64 {name}: tokens={wl.ntok} Hq={wl.Hq} Hkv={wl.Hkv}")
+    t = inputs.make_tensors(wl)
+    e = wl.evict_at()
+    cu = wl.cu_seqlens() if wl.varlen else None
+    dev_in = _device_inputs(wl)
+    res = _run(kvs, wl, dev_in)
+    for key in ("O", "LSE", "dq", "dk", "dv"):
+        assert torch.isfinite(res[key].float()).all(), f"{name} D=64: non-finite {key}"
+    for flags in (kvs.FLAG_NO_EMPTY_SKIP, kvs.FLAG_FULL_AS_PARTIAL):
+        other = _run(kvs, wl, dev_in, flags=flags)
+        for key in ("O", "LSE", "dq", "dk", "dv"):
+            a, b = res[key], other[key]
+            if a.dtype == torch.bfloat16:
+                a, b = a.view(torch.int16), b.view(torch.int16)
+            assert torch.equal(a, b), f"{name} D=64: {key} differs bitwise with flags {flags}"
+        del other
+    rows = gold["rows"]
+    ref = orc.rows_reference(t["q"], t["k"], t["v"], e, wl.softmax_scale, t["do"], rows, cu_seqlens=cu)
+    rows_t = torch.from_numpy(rows).cuda()
+    assert_close(f"{name} D=64:O", to_f64(res["O"].index_select(0, rows_t)), ref["O"])
+    assert_close(f"{name} D=64:dQ", to_f64(res["dq"].index_select(0, rows_t)), ref["dq"], E=ref["E"])
+    assert_lse(f"{name} D=64", to_f64(res["LSE"].index_select(1, rows_t)), ref["LSE"])
+    pick = _fewest_rows_keys(gold["keys"], e, cu, wl.ntok)
+    dk_ref, dv_ref = orc.keys_reference(t["q"], t["k"], t["v"], e, wl.softmax_scale, t["do"], pick, cu_seqlens=cu)
+    keys_t = torch.from_numpy(pick).cuda()
+    assert_close(f"{name} D=64:dK", to_f64(res["dk"].index_select(0, keys_t)), dk_ref)
+    assert_close(f"{name} D=64:dV", to_f64(res["dv"].index_select(0, keys_t)), dv_ref)
