@@ -10,7 +10,7 @@ Prints one JSON line.  The value is timed over exactly K steps with nothing
 else on the stream.  The same K steps are then run again with HIP events
 around every kernel on its launch stream: for the kernel that takes the most
 time, its algorithmic FLOPs per launch over its average launch duration
-("roofline").  Also the fp64 CPU checker timed on a bounded sample of the
+("roofline").  Also the fp64 CPU oracle timed on a bounded sample of the
 same workload ("cpu_baseline").
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu]
@@ -377,7 +377,7 @@ def cp_shard_bench(wl, tensors, evict_at, n_shards, warmup, steps, full_ms):
 
 
 def cpu_baseline(wl, tensors, evict_at, min_seconds=10.0):
-    """The fp64 checker as it stands, timed one q-head at a time (with its KV
+    """The fp64 oracle as it stands, timed one q-head at a time (with its KV
     head) over the whole workload until at least `min_seconds` have passed."""
     from oracle import attention as orc
 
@@ -411,7 +411,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="trace16k_gqa4")
-    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU checker timing")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle timing")
     ap.add_argument("--no-reprefill", action="store_true", help="skip the re-prefill comparison")
     ap.add_argument("--no-decode", action="store_true", help="skip the paged-cache decode measurement")
     ap.add_argument("--cp-shards", type=int, default=0,

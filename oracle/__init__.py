@@ -1,4 +1,4 @@
-"""CPU checker for eviction-masked attention (test infrastructure only).
+"""CPU oracle for eviction-masked attention (test infrastructure only).
 
 This package is the plain, slow, obviously correct definition of what the
 HIP library computes.  Only the test suite, the smoke check and the CPU

@@ -1,7 +1,7 @@
 """Seeded synthetic inputs for eviction-masked attention.
 
 This module builds the two kinds of input that both the HIP path and the
-CPU checker consume, and nothing else: the per-key eviction index
+CPU oracle consume, and nothing else: the per-key eviction index
 ``evict_at`` of a compacted agent trace, and seeded bf16 Q/K/V/dO tensors.
 It holds none of the attention arithmetic.
 

@@ -1,15 +1,15 @@
-"""Write the sampled expected outputs of the full-size workloads (CPU checker only).
+"""Write the sampled expected outputs of the full-size workloads (CPU oracle only).
 
     python tests/golden/make_parity_fixtures.py [workload ...]
 
-For each workload the fp64 checker runs forward + backward for the q-heads of
+For each workload the fp64 oracle runs forward + backward for the q-heads of
 the first and the last KV head (0 and Hkv - 1) over the whole workload (every
 trace, every row), and the script stores, as float32:
 
 * O, LSE, dQ of those q-heads at a set of sampled query rows that covers the
   prompt, every kind of segment boundary, summaries and the trace ends;
 * dK, dV of those KV heads at a set of sampled keys chosen the same way;
-* at the sampled rows, the checker's first-order sensitivity of dQ to the
+* at the sampled rows, the oracle's first-order sensitivity of dQ to the
   roundings of Delta and dS (``oracle.attention.dq_rounding_scale``), which
   enters the dQ tolerance;
 * the whole-tensor norm of each of O, dQ, dK, dV per KV head.

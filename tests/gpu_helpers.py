@@ -4,7 +4,7 @@ import sys
 import numpy as np
 import torch
 
-# Parity bar for bf16 outputs against the fp64 checker, per element
+# Parity bar for bf16 outputs against the fp64 oracle, per element
 #     |x - x*| <= MAX_ABS + ULP_FACTOR * ulp_bf16(x*)                         (O)
 #     |x - x*| <= MAX_ABS + ULP_FACTOR * ulp_bf16(x*) + DQ_GAMMA * E           (dQ)
 #     |x - x*| <= MAX_ABS + ULP_FACTOR * ulp_bf16(x*) + RSS_LAMBDA * U * S     (dK, dV)
@@ -14,7 +14,7 @@ import torch
 # cannot allow for.  ULP_FACTOR comes from the CPU model of the kernels'
 # roundings (tests/kernel_model.py): at least the model's largest excess over
 # the rest of the bound and at most twice it (tests/test_kernel_model.py).
-# E = oracle.attention.dq_rounding_scale is the checker's first-order
+# E = oracle.attention.dq_rounding_scale is the oracle's first-order
 # sensitivity of dQ to the bf16 roundings of O (through Delta) and of dS,
 # DQ_GAMMA = 2^-8 the relative rounding bound of bf16.  S =
 # oracle.attention.dkdv_rounding_rss is the root sum of squares of the terms of

@@ -1,6 +1,6 @@
-"""CPU model of the HIP kernels' arithmetic (test infrastructure, not the checker).
+"""CPU model of the HIP kernels' arithmetic (test infrastructure, not the oracle).
 
-The fp64 checker in ``oracle/`` defines what the library computes.  This
+The fp64 oracle in ``oracle/`` defines what the library computes.  This
 module replays, in numpy, the precision choices the gfx950 kernels make on the
 way there, so that the tests can tell how far a kernel with exactly these
 roundings lies from the exact result, and so derive the parity bound from the

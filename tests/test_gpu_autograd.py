@@ -2,7 +2,7 @@
 
 Gradients through ``torch.autograd`` must be exactly those of the explicit
 forward and backward calls (same kernels, same inputs), and match the fp64
-checker; LSE is returned without a gradient.  Every case prints its name
+oracle; LSE is returned without a gradient.  Every case prints its name
 before it runs.
 """
 import numpy as np
@@ -26,7 +26,7 @@ def kvs():
 
 
 @pytest.mark.parametrize("varlen", [False, True], ids=["fixed", "varlen"])
-def test_autograd_matches_explicit_calls_and_checker(kvs, varlen):
+def test_autograd_matches_explicit_calls_and_oracle(kvs, varlen):
     lengths = [300, 300] if not varlen else [257, 1, 130]
     wl = inputs.custom_workload("autograd", 8, 2, 128, lengths, 12, 60, 10, "last2", varlen=varlen, seed=61)
     announce(f"autograd {wl.name} lengths={lengths} varlen={varlen}")

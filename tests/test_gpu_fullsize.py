@@ -1,11 +1,11 @@
 """Full-size workloads: the HIP path at the exact launch configuration the
-benchmark times, compared with the fp64 checker at sampled positions, and the
+benchmark times, compared with the fp64 oracle at sampled positions, and the
 tile-classifier shortcuts checked bit for bit over the whole tensors.
 
 The expected values come from ``tests/golden/make_parity_fixtures.py`` (which
-runs only the checker, for the q-heads of the first and the last KV head).
+runs only the oracle, for the q-heads of the first and the last KV head).
 Bound (tests/gpu_helpers.py): |x - x*| <= 2e-2 + 0.45 ulp_bf16(x*) per
-element (+ 2^-8 E for dQ, E the checker's first-order sensitivity of dQ to
+element (+ 2^-8 E for dQ, E the oracle's first-order sensitivity of dQ to
 the bf16 roundings of O and dS) and relative L2 <= 1e-2 for O, dQ, dK, dV;
 LSE within 1e-3 absolute.  Every comparison prints its flat max |x - x*|
 against 2e-2, its worst error / bound and its relative L2.
@@ -91,7 +91,7 @@ def test_fullsize_sampled_parity(kvs, name):
     assert_close(f"{name}:dK", pick(res["dk"], keys_t, kvh_t), gold["dK"])
     assert_close(f"{name}:dV", pick(res["dv"], keys_t, kvh_t), gold["dV"])
     assert_lse(name, to_f64(res["LSE"].index_select(0, heads_t).index_select(1, rows_t)), gold["LSE"])
-    # whole-tensor norms of each checked KV head's outputs (every row, every key) against the checker's
+    # whole-tensor norms of each checked KV head's outputs (every row, every key) against the oracle's
     for i, g in enumerate(gold["kv_heads"]):
         hs = slice(g * G, (g + 1) * G)
         for key, gkey, sl in (("O", "norm_O", hs), ("dq", "norm_dQ", hs), ("dk", "norm_dK", slice(g, g + 1)),
@@ -134,7 +134,7 @@ def test_fullsize_every_head_sampled(kvs, name):
     """Every q-head and every KV head at the benchmarked launch configuration:
     O, LSE and dQ at the fixture's sampled rows for all q-heads, and dK, dV for
     all KV heads at the sampled keys seen by the fewest rows, against the
-    checker's row- and key-sampled forms evaluated here."""
+    oracle's row- and key-sampled forms evaluated here."""
     path = os.path.join(GOLDEN, f"parity_{name}.npz")
     if not os.path.exists(path):
         pytest.skip(f"{path} not generated")
@@ -162,7 +162,7 @@ def test_fullsize_every_head_sampled(kvs, name):
 def test_fullsize_head_dim_64(kvs, name):
     """The D = 64 kernels at full size (same layouts, head dimension 64): every
     q-head at the fixture's sampled rows, every KV head at the sampled keys
-    seen by the fewest rows, against the sampled checker; finiteness and the
+    seen by the fewest rows, against the sampled oracle; finiteness and the
     tile-classifier switches bit for bit over the whole tensors."""
     import dataclasses
 

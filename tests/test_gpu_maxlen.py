@@ -6,7 +6,7 @@ At this length the key blocks of the prompt stay visible to every one of
 some of them run as single long work items; the row kernels' tile walkers
 skip thousands of empty key tiles per row block; every grid, workspace and
 offset is at its largest for one trace.  The expected values come from the
-fp64 checker evaluated at sampled rows and keys only (each row over its own
+fp64 oracle evaluated at sampled rows and keys only (each row over its own
 visible set: ``oracle.attention.rows_reference`` / ``keys_reference``); keys
 that every row sees (the prompt) are outside what it can sum in a test's
 time and are covered by the whole-tensor finiteness check and by the

@@ -1,6 +1,6 @@
-"""HIP path vs the fp64 checker, element by element, on seeded inputs (MI355X).
+"""HIP path vs the fp64 oracle, element by element, on seeded inputs (MI355X).
 
-Sizes here are ones the checker finishes in seconds while still spanning
+Sizes here are ones the oracle finishes in seconds while still spanning
 several tiles and ragged tails.  Every case prints its name before it runs.
 """
 import numpy as np
@@ -26,7 +26,7 @@ def kvs():
 
 
 def _parity(kvs, wl, e, cu=None, B=None, switches=True, q_mul=None):
-    """Element by element against the checker; then the tile-classifier
+    """Element by element against the oracle; then the tile-classifier
     switches must leave every output bit-identical.  q_mul (a power of two, so
     the bf16 query stays exact) widens the logits."""
     t = inputs.make_tensors(wl)

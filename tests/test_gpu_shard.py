@@ -7,7 +7,7 @@ and every local key's dK/dV is added into its owner's row (the backward's
 reduce-scatter).  The assembled result must meet the parity bar against the
 fp64 oracle of the whole trace: at small size element by element, at full
 size (64k tokens, last-2 summaries, 8 shards at segment starts) at the
-sampled positions of the committed checker fixture.
+sampled positions of the committed oracle fixture.
 """
 import math
 import os

@@ -1,9 +1,9 @@
 """The CPU model of the kernels' arithmetic (``tests/kernel_model.py``), and the
 parity bound derived from it.
 
-* The model is the checker's computation up to the kernels' roundings: it
+* The model is the oracle's computation up to the kernels' roundings: it
   meets the stated bar (max |x - x*| <= 2e-2 where bf16 spacing allows it,
-  relative L2 <= 1e-2) against the fp64 checker.
+  relative L2 <= 1e-2) against the fp64 oracle.
 * Replaying the forward's tile walk and its wave-wide rescale decision on a
   layout without a permanent prompt (Section 2 segments with p = 0: the first
   keys are evicted) shows why the rescale factor needs its guard: without it
@@ -12,7 +12,7 @@ parity bound derived from it.
 * The parity bound of the GPU tests is |x - x*| <= 2e-2 + C ulp_bf16(x*)
   (+ 2^-8 E for dQ, below).  C comes from the model: the largest excess over
   the rest of the bound, in units of the bf16 spacing at x*, over workloads
-  shaped like the benchmark configurations (scaled down so that the checker
+  shaped like the benchmark configurations (scaled down so that the oracle
   finishes in seconds) must be at most C, and C at most twice that excess.
   The excess is the final rounding: a bf16 output between 8 and 16 is up to
   1/32 from the exact value, more than 2e-2.

@@ -1,6 +1,6 @@
 """The pins are discriminating: planting a plausible mistake in a copy of the
-CPU checker (a dropped term, a wrong sign, index or boundary, a missing scale)
-makes at least one pin fail.  CPU only; the checker itself is untouched."""
+CPU oracle (a dropped term, a wrong sign, index or boundary, a missing scale)
+makes at least one pin fail.  CPU only; the oracle itself is untouched."""
 import math
 import os
 import types
@@ -88,7 +88,7 @@ def _pins(orc):
     np.testing.assert_allclose(sv, vt.grad.numpy(), rtol=1e-9, atol=1e-10)
 
 
-def test_unmutated_checker_passes_battery():
+def test_unmutated_oracle_passes_battery():
     _pins(_load(SRC))
 
 

@@ -1,6 +1,6 @@
-"""Pins of the fp64 CPU checker against facts that do not come from itself.
+"""Pins of the fp64 CPU oracle against facts that do not come from itself.
 
-Each test ties the checker (``oracle/``) to something else the paper or the
+Each test ties the oracle (``oracle/``) to something else the paper or the
 mathematics fixes: causal attention from a library routine, a token-by-token
 replay of the streamed KV cache, finite differences, closed forms and hand
 counts.  No GPU.
@@ -342,7 +342,7 @@ TURN_CASES = [
 def test_turn_strategies_match_stream_replay(case):
     """The closed-form eviction indices of the turn-level generators equal the
     ones implied by an event-driven replay of the streamed cache, and one
-    masked pass of the checker equals attention over the replayed live sets
+    masked pass of the oracle equals attention over the replayed live sets
     (forward and gradients)."""
     p, n, lo, hi, pad, strategy, window, stride, keep, seed = case
     rng = np.random.default_rng(seed)
@@ -387,7 +387,7 @@ def test_dq_rounding_scale_closed_forms():
     * Row 1 of a causal trace sees two keys: dS_10 = -dS_11 = P_10 P_11 (dP_10 - dP_11),
       so the dS part is scale |dS_10| (|k_0d| + |k_1d|).
     * The Delta part's sum_j P_ij k_j is attention with the keys as values: the
-      checker's forward with V := K.
+      oracle's forward with V := K.
     """
     rng = np.random.default_rng(5)
     L, Hq, Hkv, D, scale = 9, 4, 2, 8, 0.37
