@@ -300,8 +300,9 @@ def _gatherable(x):
 
 
 def _widen(a: np.ndarray) -> np.ndarray:
-    """fp64 values of gathered elements: bf16 bit patterns become the fp32 with
-    those upper 16 bits (exact), widened to fp64; floats are widened."""
+    """fp64 values of elements gathered from ``_gatherable``: its int16 arrays
+    hold bf16 bit patterns, which become the fp32 with those upper 16 bits
+    (exact), widened to fp64; floats are widened."""
     if a.dtype == np.int16:
         return (a.astype(np.int32) << 16).view(np.float32).astype(np.float64)
     return np.asarray(a, dtype=np.float64)
@@ -337,6 +338,8 @@ def rows_reference(q, k, v, evict_at, scale, do, rows, cu_seqlens=None):
     out = {"O": np.zeros((rows.size, Hq, D)), "dq": np.zeros((rows.size, Hq, D)), "E": np.zeros((rows.size, Hq, D)),
            "LSE": np.zeros((Hq, rows.size)), "Delta": np.zeros((Hq, rows.size))}
     qr, kr, vr, dor = (_gatherable(x) for x in (q, k, v, do))
+    for a, b in _split(cu_seqlens, n):
+        check_evict_at(e[a:b], b - a)
     for r, pos in enumerate(rows):
         a, b = _trace_of(int(pos), cu_seqlens, n)
         js = a + _visible_keys(e[a:b], b - a, int(pos) - a)
@@ -384,6 +387,7 @@ def keys_reference(q, k, v, evict_at, scale, do, keys, cu_seqlens=None):
         mine = np.nonzero((keys >= a) & (keys < b))[0]
         if mine.size == 0:
             continue
+        check_evict_at(e[a:b], L)
         et = np.minimum(e[a:b], L)
         rows = np.unique(np.concatenate([np.arange(keys[c] - a, et[keys[c] - a]) for c in mine]))
         runs = np.split(rows, np.nonzero(np.diff(rows) > 1)[0] + 1)   # consecutive rows

@@ -320,8 +320,13 @@ def test_sampled_forms_match_replay_and_closed_forms():
 
 def test_invalid_evict_at_rejected():
     q = _rand((5, 1, 8), 1)
+    bad = np.array([1, 2, 2, 5, 5])
     with pytest.raises(ValueError):
-        orc.forward(q, q, q, np.array([1, 2, 2, 5, 5]), 1.0)
+        orc.forward(q, q, q, bad, 1.0)
+    with pytest.raises(ValueError):
+        orc.rows_reference(q, q, q, bad, 1.0, q, [4])
+    with pytest.raises(ValueError):
+        orc.keys_reference(q, q, q, bad, 1.0, q, [0])
 
 
 # ---------------------------------------------------------------- turn-level strategies (Section 3)
