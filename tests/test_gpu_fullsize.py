@@ -17,6 +17,7 @@ shortcuts are checked exactly: the same calls with every EMPTY tile processed
 (masked) and with every FULL tile masked must give bit-identical O, LSE, dQ,
 dK and dV over the whole tensors.
 """
+import dataclasses
 import os
 
 import numpy as np
@@ -164,8 +165,6 @@ def test_fullsize_head_dim_64(kvs, name):
     q-head at the fixture's sampled rows, every KV head at the sampled keys
     seen by the fewest rows, against the sampled oracle; finiteness and the
     tile-classifier switches bit for bit over the whole tensors."""
-    import dataclasses
-
     gold = np.load(os.path.join(GOLDEN, f"parity_{name}.npz"))
     wl = dataclasses.replace(inputs.WORKLOADS[name], D=64)
     announce(f"full-size D=64 {name}: tokens={wl.ntok} Hq={wl.Hq} Hkv={wl.Hkv}")
