@@ -25,16 +25,18 @@ def kvs():
     return k
 
 
-def _parity(kvs, wl, e, cu=None, B=None, switches=True, q_mul=None):
+def _parity(kvs, wl, e, cu=None, B=None, switches=True, q_mul=None, max_seqlen=None):
     """Element by element against the oracle; then the tile-classifier
     switches must leave every output bit-identical.  q_mul (a power of two, so
-    the bf16 query stays exact) widens the logits."""
+    the bf16 query stays exact) widens the logits; max_seqlen (varlen) may
+    exceed the longest trace."""
     t = inputs.make_tensors(wl)
     if q_mul is not None:
         t["q"] = t["q"] * q_mul
     scale = wl.softmax_scale
-    announce(f"{wl.name} lengths={wl.lengths} Hq={wl.Hq} Hkv={wl.Hkv} D={wl.D} varlen={cu is not None} B={B}")
-    mx = max(wl.lengths) if cu is not None else None
+    mx = (max_seqlen or max(wl.lengths)) if cu is not None else None
+    announce(f"{wl.name} lengths={wl.lengths} Hq={wl.Hq} Hkv={wl.Hkv} D={wl.D} varlen={cu is not None} B={B} "
+             f"max_seqlen={mx}")
     res = gpu_fwd_bwd(kvs, t["q"], t["k"], t["v"], t["do"], e, scale, cu_seqlens=cu, max_seqlen=mx, B=B)
     cu_ref = cu if cu is not None else (np.arange(B + 1) * wl.lengths[0] if B else None)
     ref = orc.backward(t["q"], t["k"], t["v"], e, scale, t["do"], cu_seqlens=cu_ref)
@@ -129,6 +131,19 @@ def test_varlen_ragged(kvs):
     wl = inputs.custom_workload("varlen_small", 10, 2, 128, [37, 1, 300, 129, 64], 4, 50, 10, "keep_all",
                                 varlen=True, seed=13)
     _parity(kvs, wl, wl.evict_at(), cu=wl.cu_seqlens())
+
+
+@pytest.mark.parametrize("D", [128, 64])
+def test_varlen_loose_max_seqlen(kvs, D):
+    """max_seqlen only bounds the trace lengths: three times the longest (grids
+    and the dK/dV plan sized for longer traces than there are) gives the same
+    parity, including split slots sized for traces that are not there."""
+    wl = inputs.custom_workload(f"varlen_loose_D{D}", 6, 2, D, [37, 1, 300, 129, 0, 64], 4, 50, 10, "latest_only",
+                                varlen=True, seed=21 + D)
+    _parity(kvs, wl, wl.evict_at(), cu=wl.cu_seqlens(), max_seqlen=3 * max(wl.lengths))
+    wl = inputs.custom_workload(f"varlen_loose_split_D{D}", 4, 2, D, [300, 1200], 64, 200, 20, "keep_all",
+                                varlen=True, seed=25 + D)
+    _parity(kvs, wl, wl.evict_at(), cu=wl.cu_seqlens(), max_seqlen=9000)
 
 
 def test_varlen_without_prompt(kvs):
