@@ -368,11 +368,12 @@ def keys_reference(q, k, v, evict_at, scale, do, keys, cu_seqlens=None):
 
     Key j of a trace is seen by the rows R(j) = [j, min(e_j, L)).  The union
     of those rows is processed once, in blocks of consecutive rows as in
-    ``backward`` (no block spans a gap), but each block's columns are only the keys some row of the
-    block can see (j <= the block's last row, min(e_j, L) > its first), with
-    the explicit mask on top: every row's P and dS, so its LSE and Delta, are
-    those of the definition.  The G q-heads of a KV head are stacked as extra
-    rows.  Returns fp64 ``dk, dv [len(keys), Hkv, D]``.
+    ``backward`` (no block spans a gap), but each block's columns are only
+    the keys some row of the block can see (j <= the block's last row,
+    min(e_j, L) > its first), with the explicit mask on top: every row's P
+    and dS, so its LSE and Delta, are those of the definition.  The G q-heads
+    of a KV head are stacked as extra rows.  Returns fp64
+    ``dk, dv [len(keys), Hkv, D]``.
     """
     e = np.asarray(evict_at, dtype=np.int64)
     keys = np.asarray(keys, dtype=np.int64)
